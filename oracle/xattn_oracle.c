@@ -21,7 +21,8 @@
  *     of the diagonal block are never candidates;
  *   - a block's score is the mean over its B/S reduced rows of the reduced
  *     softmax mass in its B/S reduced columns (each query-block row sums to 1);
- *   - find_blocks: masses are taken as integers u_j = floor(score_j * 2^32),
+ *   - find_blocks: masses are taken as integers u_j = floor(score_j * 2^32)
+ *     (score clamped to [0, 1]),
  *     the row total T = sum u_j, the target ceil(tau * T) (one IEEE fp64
  *     product), candidates ordered by (u desc, j asc), the shortest prefix of
  *     length >= 1 whose integer cumulative sum reaches the target; tau >= 1
@@ -152,7 +153,8 @@ void oracle_select_rows(const double *scores, int NB, int causal, int nrows,
         cand *c = (cand *)malloc(sizeof(cand) * m);
         uint64_t total = 0;
         for (int j = 0; j < m; ++j) {
-            double v = s[j] > 0.0 ? s[j] : 0.0;
+            /* a block mass lies in [0, 1]; NaN counts as 0 */
+            double v = s[j] > 0.0 ? (s[j] < 1.0 ? s[j] : 1.0) : 0.0;
             c[j].u = (uint64_t)floor(v * 4294967296.0);
             c[j].j = j;
             total += c[j].u;

@@ -177,7 +177,7 @@ def test_fig1_geometry():
 
 
 def _units(s):
-    return np.floor(np.maximum(s.astype(np.float64), 0.0) * 2.0 ** 32).astype(np.uint64)
+    return np.floor(np.clip(s.astype(np.float64), 0.0, 1.0) * 2.0 ** 32).astype(np.uint64)
 
 
 @pytest.mark.parametrize("seed,ties", [(1, False), (2, False), (3, True), (4, True)])
@@ -222,6 +222,15 @@ def test_select_small_integer_masses_match_subset_enumeration():
                                              for c in itertools.combinations(range(NB), size)))
             assert cnt[r] == best, (tau, u)
             assert sum(u[j] for j in idx[r, :cnt[r]]) >= thr or cnt[r] == NB
+
+
+def test_select_clamps_masses_to_unit_interval():
+    # A block mass is at most 1: larger values count as 1, negative or NaN as 0.
+    s = np.array([[3.0, 1.0, 0.5, -2.0, np.nan, 0.5]], np.float32)
+    idx, cnt = oracle.select_rows(s, np.array([5], np.int32), 0.7, causal=False)
+    # units: [2^32, 2^32, 2^31, 0, 0, 2^31], T = 3 * 2^32, target = 0.7 T
+    # -> two blocks of 2^32 (2/3 of T) fall short, the third (2^31, j=2) reaches it
+    assert cnt[0] == 3 and idx[0, :3].tolist() == [0, 1, 2]
 
 
 def test_select_tau_one_takes_every_candidate_even_zero_mass():
