@@ -1,0 +1,159 @@
+/*
+ * xattn.h -- C ABI of the MI355X (gfx950) XAttention prefill library.
+ *
+ * XAttention (arXiv 2503.16428) replaces dense prefill attention by three
+ * steps (Fig. 1): (1) strided antidiagonal block scoring, (2) threshold block
+ * selection, (3) attention on the selected blocks only. Each step is one call
+ * here, plus a dense reference mode and a chained forward.
+ *
+ * Conventions shared by every call
+ *   - Plain C; no HIP or torch types. `stream` is a hipStream_t passed as
+ *     void* (NULL = the default stream). Every call only validates its
+ *     arguments on the host and enqueues kernels on `stream`: it never
+ *     allocates, never synchronises and never throws. Results are ready when
+ *     the caller synchronises the stream.
+ *   - All array pointers are DEVICE pointers owned by the caller; the library
+ *     keeps none of them after the call returns. Arrays are dense and
+ *     row-major in the shapes stated below; tensors of bfloat16 values are
+ *     passed as `const void*`.
+ *   - Heads: query head h (0 <= h < batch*hq) reads key/value head
+ *     (h / hq) * hkv + (h % hq) / (hq / hkv)  (contiguous GQA grouping).
+ *   - Shapes use L = dims->seq, D = dims->head_dim, NB = L / block,
+ *     HQ = batch * hq, HKV = batch * hkv.
+ *   - Return value: XATTN_OK or an error code; on error nothing has been
+ *     enqueued (argument errors) or the HIP launch failed (XATTN_ERR_HIP).
+ *     xattn_last_error() gives a message for the calling thread.
+ *   - Results are deterministic: the same inputs give bitwise equal outputs.
+ *
+ * Supported today: head_dim 128, block 128, stride S in {1,2,4,8,16,32,64},
+ * seq a multiple of 128 and at most 262144 (NB <= 2048).
+ */
+#ifndef XATTN_H
+#define XATTN_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+enum xattn_status {
+    XATTN_OK = 0,
+    XATTN_ERR_ARG = 1,          /* invalid argument (null pointer, bad shape, tau <= 0 or NaN) */
+    XATTN_ERR_UNSUPPORTED = 2,  /* valid but not implemented (e.g. head_dim != 128) */
+    XATTN_ERR_WORKSPACE = 3,    /* workspace pointer null or smaller than required */
+    XATTN_ERR_HIP = 4           /* a HIP runtime call or kernel launch failed */
+};
+
+/* Problem shape. Layouts: Q [batch][hq][seq][head_dim], K and V
+ * [batch][hkv][seq][head_dim], all bfloat16. causal: 1 = query i attends to
+ * keys k <= i (decoder prefill), 0 = bidirectional (e.g. video DiT). */
+typedef struct xattn_dims {
+    int32_t batch;
+    int32_t hq;
+    int32_t hkv;
+    int32_t seq;
+    int32_t head_dim;
+    int32_t causal;
+} xattn_dims;
+
+/*
+ * Step 1 -- strided antidiagonal block scoring (Sec. 3.1-3.2, Algorithm 1).
+ *
+ * For query head h, query block b and key block j, with nr = block / stride
+ * reduced rows per block and reduced row R = b*nr + r:
+ *   x[R][c]  = (1 / (sqrt(D) * S)) * sum_{t<S} q[R*S + S-1-t] . k[c*S + t]
+ *              (the product of Algorithm 1's strided reshapes: the sum over
+ *              the antidiagonal of every S x S sub-block of Q K^T),
+ *   A[R][c]  = softmax over the valid reduced columns c (c <= R when causal),
+ *   scores[h][b][j] = (1/nr) * sum_{r<nr} sum_{c in block j} A[R][c],
+ * so every row sums to 1. Entries with j > b (causal) are written as 0.
+ *   q        bf16 [HQ][L][D]          k  bf16 [HKV][L][D]
+ *   scores   fp32 [HQ][NB][NB]        (output, fully written)
+ *   workspace  device scratch of at least xattn_score_workspace_size() bytes;
+ *              its contents on entry are ignored, on exit unspecified.
+ * Products are bf16 x bf16 on the matrix cores with fp32 accumulation; the
+ * softmax and block sums are fp32.
+ */
+int xattn_score_workspace_size(const xattn_dims *dims, int block, int stride,
+                               size_t *bytes);
+int xattn_score(const void *q, const void *k, const xattn_dims *dims, int block,
+                int stride, float *scores, void *workspace, size_t workspace_bytes,
+                void *stream);
+
+/*
+ * Step 2 -- threshold block selection, find_blocks (Sec. 3.2, equation of
+ * find_blocks; Algorithm 1). Per row (h, b) the candidates are j <= b
+ * (causal) or all j. Each candidate's mass is taken as the integer
+ * u_j = floor(clamp(scores[h][b][j], 0, 1) * 2^32); T = sum of u_j over the
+ * candidates. The selected set is the shortest prefix (length >= 1) of the
+ * candidates ordered by (u_j descending, j ascending) whose integer sum
+ * reaches ceil(tau * T) (tau * T as one fp64 product). tau >= 1 selects every
+ * candidate. Integer masses make the result independent of summation order.
+ *   scores  fp32 [HQ][NB][NB]   (input; only candidate entries are read)
+ *   tau     threshold, 0 < tau; values >= 1 mean "all candidates"
+ *   idx     int32 [HQ][NB][NB]  (output) row (h, b): idx[h][b][0 .. cnt) are
+ *           the selected key blocks in ascending order; later entries are
+ *           left unchanged
+ *   cnt     int32 [HQ][NB]      (output) number selected, >= 1
+ */
+int xattn_select(const float *scores, const xattn_dims *dims, int block, float tau,
+                 int32_t *idx, int32_t *cnt, void *stream);
+
+/*
+ * Step 3 -- block-sparse attention (Fig. 1, right): for query i in block b of
+ * head h, with K_i the keys of the listed key blocks idx[h][b][0 .. cnt)
+ * (intersected with k <= i when causal):
+ *   o[h][i]   = sum_{k in K_i} softmax_k(q_i . k_k / sqrt(D)) v_k
+ *   lse[h][i] = log sum_{k in K_i} exp(q_i . k_k / sqrt(D))   (natural log)
+ * A query with no visible key gets o = 0 and lse = -inf. Lists must hold
+ * distinct ascending block indices in [0, NB); cnt in [0, NB].
+ *   q  bf16 [HQ][L][D]; k, v bf16 [HKV][L][D]
+ *   idx int32 [HQ][NB][NB], cnt int32 [HQ][NB]  (e.g. from xattn_select)
+ *   o   bf16 [HQ][L][D] (output)
+ *   lse fp32 [HQ][L] (output) or NULL
+ * QK^T and PV run on the bf16 matrix cores with fp32 accumulation; the
+ * online softmax is fp32 and P is rounded to bf16 for the PV product.
+ */
+int xattn_block_sparse_attn(const void *q, const void *k, const void *v,
+                            const xattn_dims *dims, int block, const int32_t *idx,
+                            const int32_t *cnt, void *o, float *lse, void *stream);
+
+/*
+ * Dense reference mode (the paper's speedup denominator, Sec. 4.3): the same
+ * kernel as xattn_block_sparse_attn with every candidate block listed
+ * (j <= b causal, all j otherwise), block 128. Bitwise equal to
+ * xattn_block_sparse_attn on the lists xattn_select returns for tau >= 1.
+ */
+int xattn_dense_attn(const void *q, const void *k, const void *v,
+                     const xattn_dims *dims, void *o, float *lse, void *stream);
+
+/*
+ * The three steps chained on one stream: score -> select -> sparse attention.
+ * workspace: at least xattn_forward_workspace_size() bytes. It holds, in
+ * order, scores fp32 [HQ][NB][NB], idx int32 [HQ][NB][NB], cnt int32 [HQ][NB]
+ * (each at a 256-byte aligned offset reported by xattn_forward_layout) and
+ * the scoring scratch; after the call the caller may read scores/idx/cnt there.
+ */
+int xattn_forward_workspace_size(const xattn_dims *dims, int block, int stride,
+                                 size_t *bytes);
+int xattn_forward_layout(const xattn_dims *dims, int block, int stride,
+                         size_t *scores_off, size_t *idx_off, size_t *cnt_off,
+                         size_t *scratch_off);
+int xattn_forward(const void *q, const void *k, const void *v, const xattn_dims *dims,
+                  int block, int stride, float tau, void *o, float *lse,
+                  void *workspace, size_t workspace_bytes, void *stream);
+
+/* Static description of a status code (never NULL). */
+const char *xattn_strerror(int status);
+/* Message describing the last failure on the calling thread ("" if none). */
+const char *xattn_last_error(void);
+/* Library ABI version: major * 10000 + minor * 100 + patch. */
+int xattn_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* XATTN_H */

@@ -1,0 +1,9 @@
+"""MI355X (gfx950) XAttention prefill path: antidiagonal block scoring,
+threshold block selection and block-sparse attention as HIP kernels behind a
+C ABI (include/xattn.h). This package holds the kernels' sources (csrc/), the
+in-tree build (build.py) and a thin ctypes binding (binding.py)."""
+from .binding import (  # noqa: F401
+    BLOCK, Dims, XAttnError, forward_layout, forward_workspace_size, lib, lib_path,
+    make_dims, score_workspace_size, version, xattn_block_sparse_attn, xattn_dense_attn,
+    xattn_forward, xattn_score, xattn_select,
+)

@@ -1,0 +1,249 @@
+"""Thin ctypes binding of libxattn.so (the C ABI declared in include/xattn.h).
+
+Argument marshalling only: tensors are torch device tensors (torch supplies
+device memory and the current HIP stream); every step of the computation runs
+in the library's HIP kernels. There is no fallback: if the library is missing
+or no GPU is present, calls raise.
+
+Tensor layouts (batch folded into heads when 3-D tensors are given):
+  q      bf16 [batch, hq, seq, 128]  or [hq, seq, 128]
+  k, v   bf16 [batch, hkv, seq, 128] or [hkv, seq, 128]
+  scores fp32 [batch*hq, NB, NB]; idx int32 [batch*hq, NB, NB]; cnt int32 [batch*hq, NB]
+  o      bf16 like q; lse fp32 [batch*hq, seq]
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+import torch
+
+from . import build as _build
+
+XATTN_OK = 0
+XATTN_ERR_ARG = 1
+XATTN_ERR_UNSUPPORTED = 2
+XATTN_ERR_WORKSPACE = 3
+XATTN_ERR_HIP = 4
+BLOCK = 128
+
+_LIB = None
+
+
+class XAttnError(RuntimeError):
+    def __init__(self, status: int, msg: str):
+        super().__init__(f"xattn status {status}: {msg}")
+        self.status = status
+
+
+class Dims(ctypes.Structure):
+    _fields_ = [("batch", ctypes.c_int32), ("hq", ctypes.c_int32), ("hkv", ctypes.c_int32),
+                ("seq", ctypes.c_int32), ("head_dim", ctypes.c_int32),
+                ("causal", ctypes.c_int32)]
+
+    def __repr__(self):
+        return (f"Dims(batch={self.batch}, hq={self.hq}, hkv={self.hkv}, seq={self.seq}, "
+                f"head_dim={self.head_dim}, causal={self.causal})")
+
+    @property
+    def n_blocks(self) -> int:
+        return self.seq // BLOCK
+
+    @property
+    def heads(self) -> int:
+        return self.batch * self.hq
+
+
+EXPORTS = [
+    "xattn_score_workspace_size", "xattn_score", "xattn_select", "xattn_block_sparse_attn",
+    "xattn_dense_attn", "xattn_forward_workspace_size", "xattn_forward_layout",
+    "xattn_forward", "xattn_strerror", "xattn_last_error", "xattn_version",
+]
+
+
+def lib_path() -> str:
+    return _build.LIB
+
+
+def lib() -> ctypes.CDLL:
+    """Load the HIP library (raises if it has not been built)."""
+    global _LIB
+    if _LIB is None:
+        if not os.path.exists(_build.LIB):
+            raise XAttnError(XATTN_ERR_HIP, f"{_build.LIB} not built; run __graft_entry__.build()")
+        L = ctypes.CDLL(_build.LIB)
+        P, I, F, SZ = ctypes.c_void_p, ctypes.c_int, ctypes.c_float, ctypes.c_size_t
+        PD = ctypes.POINTER(Dims)
+        PSZ = ctypes.POINTER(SZ)
+        L.xattn_score_workspace_size.argtypes = [PD, I, I, PSZ]
+        L.xattn_score.argtypes = [P, P, PD, I, I, P, P, SZ, P]
+        L.xattn_select.argtypes = [P, PD, I, F, P, P, P]
+        L.xattn_block_sparse_attn.argtypes = [P, P, P, PD, I, P, P, P, P, P]
+        L.xattn_dense_attn.argtypes = [P, P, P, PD, P, P, P]
+        L.xattn_forward_workspace_size.argtypes = [PD, I, I, PSZ]
+        L.xattn_forward_layout.argtypes = [PD, I, I, PSZ, PSZ, PSZ, PSZ]
+        L.xattn_forward.argtypes = [P, P, P, PD, I, I, F, P, P, P, SZ, P]
+        L.xattn_strerror.argtypes = [I]
+        L.xattn_strerror.restype = ctypes.c_char_p
+        L.xattn_last_error.restype = ctypes.c_char_p
+        L.xattn_version.restype = I
+        for name in EXPORTS:
+            if name not in ("xattn_strerror", "xattn_last_error", "xattn_version"):
+                getattr(L, name).restype = I
+        _LIB = L
+    return _LIB
+
+
+def _check(status: int):
+    if status != XATTN_OK:
+        L = lib()
+        raise XAttnError(status, f"{L.xattn_strerror(status).decode()}: "
+                                 f"{L.xattn_last_error().decode()}")
+
+
+def make_dims(q: torch.Tensor, k: torch.Tensor, causal: bool) -> Dims:
+    if q.dim() == 3:
+        batch, hq, seq, d = 1, q.shape[0], q.shape[1], q.shape[2]
+        hkv = k.shape[0]
+    elif q.dim() == 4:
+        batch, hq, seq, d = q.shape
+        hkv = k.shape[1]
+    else:
+        raise XAttnError(XATTN_ERR_ARG, f"q must be 3-D or 4-D, got {tuple(q.shape)}")
+    return Dims(batch, hq, hkv, seq, d, 1 if causal else 0)
+
+
+def _ptr(t):
+    return None if t is None else ctypes.c_void_p(t.data_ptr())
+
+
+def _stream(stream):
+    if stream is None:
+        stream = torch.cuda.current_stream()
+    return ctypes.c_void_p(stream.cuda_stream)
+
+
+def _need(t: torch.Tensor, dtype, name: str):
+    if not t.is_cuda:
+        raise XAttnError(XATTN_ERR_ARG, f"{name} must be a device tensor")
+    if t.dtype != dtype:
+        raise XAttnError(XATTN_ERR_ARG, f"{name} must be {dtype}, got {t.dtype}")
+    if not t.is_contiguous():
+        raise XAttnError(XATTN_ERR_ARG, f"{name} must be contiguous")
+
+
+def score_workspace_size(dims: Dims, block: int, stride: int) -> int:
+    n = ctypes.c_size_t(0)
+    _check(lib().xattn_score_workspace_size(ctypes.byref(dims), block, stride, ctypes.byref(n)))
+    return n.value
+
+
+def forward_workspace_size(dims: Dims, block: int, stride: int) -> int:
+    n = ctypes.c_size_t(0)
+    _check(lib().xattn_forward_workspace_size(ctypes.byref(dims), block, stride, ctypes.byref(n)))
+    return n.value
+
+
+def forward_layout(dims: Dims, block: int, stride: int) -> dict:
+    v = [ctypes.c_size_t(0) for _ in range(4)]
+    _check(lib().xattn_forward_layout(ctypes.byref(dims), block, stride,
+                                      *[ctypes.byref(x) for x in v]))
+    return dict(zip(("scores", "idx", "cnt", "scratch"), (x.value for x in v)))
+
+
+def xattn_score(q, k, causal=True, block=BLOCK, stride=8, scores=None, workspace=None,
+                stream=None):
+    """Antidiagonal block scores [batch*hq, NB, NB] (fp32)."""
+    _need(q, torch.bfloat16, "q")
+    _need(k, torch.bfloat16, "k")
+    d = make_dims(q, k, causal)
+    nb = d.seq // block if block > 0 else 0
+    if scores is None:
+        scores = torch.empty((d.heads, nb, nb), dtype=torch.float32, device=q.device)
+    _need(scores, torch.float32, "scores")
+    if workspace is None:
+        workspace = torch.empty(score_workspace_size(d, block, stride), dtype=torch.uint8,
+                                device=q.device)
+    _check(lib().xattn_score(_ptr(q), _ptr(k), ctypes.byref(d), block, stride, _ptr(scores),
+                             _ptr(workspace), workspace.numel(), _stream(stream)))
+    return scores
+
+
+def xattn_select(scores, dims: Dims, tau: float, block=BLOCK, idx=None, cnt=None, stream=None):
+    """find_blocks per row: (idx [H, NB, NB] int32, cnt [H, NB] int32)."""
+    _need(scores, torch.float32, "scores")
+    nb = dims.seq // block
+    if idx is None:
+        idx = torch.full((dims.heads, nb, nb), -1, dtype=torch.int32, device=scores.device)
+    if cnt is None:
+        cnt = torch.empty((dims.heads, nb), dtype=torch.int32, device=scores.device)
+    _need(idx, torch.int32, "idx")
+    _need(cnt, torch.int32, "cnt")
+    _check(lib().xattn_select(_ptr(scores), ctypes.byref(dims), block, float(tau), _ptr(idx),
+                              _ptr(cnt), _stream(stream)))
+    return idx, cnt
+
+
+def xattn_block_sparse_attn(q, k, v, idx, cnt, causal=True, block=BLOCK, o=None, lse=None,
+                            want_lse=True, stream=None):
+    """Attention over the listed key blocks: (o bf16 like q, lse fp32 [H, seq] or None)."""
+    for t, n in ((q, "q"), (k, "k"), (v, "v")):
+        _need(t, torch.bfloat16, n)
+    _need(idx, torch.int32, "idx")
+    _need(cnt, torch.int32, "cnt")
+    d = make_dims(q, k, causal)
+    if o is None:
+        o = torch.empty_like(q)
+    if lse is None and want_lse:
+        lse = torch.empty((d.heads, d.seq), dtype=torch.float32, device=q.device)
+    _check(lib().xattn_block_sparse_attn(_ptr(q), _ptr(k), _ptr(v), ctypes.byref(d), block,
+                                         _ptr(idx), _ptr(cnt), _ptr(o), _ptr(lse),
+                                         _stream(stream)))
+    return o, lse
+
+
+def xattn_dense_attn(q, k, v, causal=True, o=None, lse=None, want_lse=True, stream=None):
+    """Dense (all candidate blocks) attention, same kernel as the sparse mode."""
+    for t, n in ((q, "q"), (k, "k"), (v, "v")):
+        _need(t, torch.bfloat16, n)
+    d = make_dims(q, k, causal)
+    if o is None:
+        o = torch.empty_like(q)
+    if lse is None and want_lse:
+        lse = torch.empty((d.heads, d.seq), dtype=torch.float32, device=q.device)
+    _check(lib().xattn_dense_attn(_ptr(q), _ptr(k), _ptr(v), ctypes.byref(d), _ptr(o),
+                                  _ptr(lse), _stream(stream)))
+    return o, lse
+
+
+def xattn_forward(q, k, v, causal=True, block=BLOCK, stride=8, tau=0.9, o=None, lse=None,
+                  workspace=None, want_lse=False, stream=None):
+    """score -> select -> sparse attention. Returns (o, lse, workspace views dict)."""
+    for t, n in ((q, "q"), (k, "k"), (v, "v")):
+        _need(t, torch.bfloat16, n)
+    d = make_dims(q, k, causal)
+    if workspace is None:
+        workspace = torch.empty(forward_workspace_size(d, block, stride), dtype=torch.uint8,
+                                device=q.device)
+    if o is None:
+        o = torch.empty_like(q)
+    if lse is None and want_lse:
+        lse = torch.empty((d.heads, d.seq), dtype=torch.float32, device=q.device)
+    _check(lib().xattn_forward(_ptr(q), _ptr(k), _ptr(v), ctypes.byref(d), block, stride,
+                               float(tau), _ptr(o), _ptr(lse), _ptr(workspace),
+                               workspace.numel(), _stream(stream)))
+    lay = forward_layout(d, block, stride)
+    nb = d.seq // block
+    views = {
+        "scores": workspace[lay["scores"]:lay["scores"] + d.heads * nb * nb * 4]
+        .view(torch.float32).view(d.heads, nb, nb),
+        "idx": workspace[lay["idx"]:lay["idx"] + d.heads * nb * nb * 4]
+        .view(torch.int32).view(d.heads, nb, nb),
+        "cnt": workspace[lay["cnt"]:lay["cnt"] + d.heads * nb * 4]
+        .view(torch.int32).view(d.heads, nb),
+    }
+    return o, lse, views
+
+
+def version() -> int:
+    return lib().xattn_version()

@@ -1,0 +1,67 @@
+// Internal helpers of the gfx950 XAttention library (not part of the ABI).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace xattn {
+
+typedef __bf16 bf16_t;
+typedef __attribute__((__vector_size__(8 * sizeof(__bf16)))) __bf16 bf16x8;
+typedef __attribute__((__vector_size__(16 * sizeof(float)))) float f32x16;
+typedef __attribute__((__vector_size__(4 * sizeof(float)))) float f32x4;
+typedef __attribute__((__vector_size__(4 * sizeof(uint32_t)))) uint32_t u32x4;
+typedef __attribute__((__vector_size__(2 * sizeof(uint32_t)))) uint32_t u32x2;
+
+constexpr int kBlock = 128;     // B: attention / selection block size
+constexpr int kHeadDim = 128;   // d
+constexpr int kWave = 64;
+constexpr int kNumXcd = 8;      // MI355X: 8 XCDs, workgroups dispatched round-robin
+constexpr float kLog2e = 1.4426950408889634f;
+
+// 32x32x16 bf16 MFMA, fp32 accumulate. Lane i supplies A[i%32][8*(i/32) .. +8]
+// and B[8*(i/32) .. +8][i%32]; accumulator register r of lane i holds
+// D[8*(r/4) + 4*(i/32) + r%4][i%32].
+__device__ __forceinline__ f32x16 mfma32(bf16x8 a, bf16x8 b, f32x16 c) {
+  return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
+}
+
+__device__ __forceinline__ bf16x8 as_bf16x8(u32x4 v) { return __builtin_bit_cast(bf16x8, v); }
+
+__device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
+
+// Round-to-nearest-even fp32 -> bf16 pair packed in one dword (lo = a, hi = b).
+__device__ __forceinline__ uint32_t pack_bf16x2(float a, float b) {
+  uint32_t ua = __builtin_bit_cast(uint32_t, a), ub = __builtin_bit_cast(uint32_t, b);
+  ua = (ua + 0x7FFFu + ((ua >> 16) & 1u)) >> 16;
+  ub = (ub + 0x7FFFu + ((ub >> 16) & 1u)) & 0xFFFF0000u;
+  return ua | ub;
+}
+
+// Bijection blockIdx -> logical work index such that the workgroups one XCD
+// receives (blockIdx % 8 == x) cover one contiguous logical range; neighbours
+// in logical order then share that XCD's L2.
+__device__ __forceinline__ int xcd_remap(int bid, int n) {
+  const int x = bid % kNumXcd, k = bid / kNumXcd;
+  const int per = n / kNumXcd, rem = n % kNumXcd;
+  return x * per + (x < rem ? x : rem) + k;
+}
+
+}  // namespace xattn
+
+// Kernel launchers (one per .hip file), called by the C ABI layer after the
+// arguments have been validated. They return hipSuccess or the launch error.
+struct XattnShape {
+  int batch, hq, hkv, seq, head_dim, causal;
+  int HQ() const { return batch * hq; }
+  int NB() const { return seq / xattn::kBlock; }
+};
+
+hipError_t launch_score(const void* q, const void* k, const XattnShape& s, int stride,
+                        float* scores, void* scratch, hipStream_t st);
+size_t score_scratch_bytes(const XattnShape& s, int stride);
+hipError_t launch_select(const float* scores, const XattnShape& s, float tau, int32_t* idx,
+                         int32_t* cnt, hipStream_t st);
+hipError_t launch_attn(const void* q, const void* k, const void* v, const XattnShape& s,
+                       const int32_t* idx, const int32_t* cnt, bool dense, void* o,
+                       float* lse, hipStream_t st);

@@ -1,0 +1,133 @@
+// Step 2: threshold block selection, find_blocks (XAttention Sec. 3.2).
+//
+// find_blocks asks for the smallest set of key blocks whose mass reaches tau.
+// Masses are integers u_j = floor(clamp(score_j, 0, 1) * 2^32), so every sum
+// below is exact and the result does not depend on summation order; the
+// target is ceil(tau * T) with T the row total (one fp64 product).
+//
+// One wave64 per (head, query block) row. Instead of sorting, the wave finds
+// the mass v* of the last block the sorted prefix needs: the largest v with
+// F(v) = sum_{u_j >= v} u_j >= target (binary search, F non-increasing).
+// The shortest prefix of the (u desc, j asc) order that reaches the target is
+// then every block with u_j > v* plus the first ceil((target - F(v*+1)) / v*)
+// blocks with u_j == v* in ascending j. Emitting in ascending j with ballot /
+// popcount yields the index list already sorted.
+#include "common.h"
+
+using namespace xattn;
+
+namespace {
+
+__device__ __forceinline__ uint64_t wave_sum_u64(uint64_t x) {
+#pragma unroll
+  for (int off = 32; off >= 1; off >>= 1) {
+    const uint32_t lo = __shfl_xor((uint32_t)x, off);
+    const uint32_t hi = __shfl_xor((uint32_t)(x >> 32), off);
+    x += ((uint64_t)hi << 32) | lo;
+  }
+  return x;
+}
+
+// NPL = candidate slots per lane (64 * NPL >= NB); lane l holds j = l + 64 i.
+template <int NPL, bool CAUSAL>
+__global__ __launch_bounds__(256) void select_kernel(const float* __restrict__ scores,
+                                                     int n_rows, int NB, float tau,
+                                                     int32_t* __restrict__ idx,
+                                                     int32_t* __restrict__ cnt) {
+  const int lane = threadIdx.x & 63;
+  const int row = blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (row >= n_rows) return;  // uniform per wave
+  const int b = row % NB;
+  const int m = CAUSAL ? b + 1 : NB;
+  const float* s = scores + (size_t)row * NB;
+  int32_t* out = idx + (size_t)row * NB;
+
+  if (tau >= 1.f) {
+    for (int j = lane; j < m; j += 64) out[j] = j;
+    if (lane == 0) cnt[row] = m;
+    return;
+  }
+
+  uint64_t u[NPL];
+  uint64_t tl = 0;
+#pragma unroll
+  for (int i = 0; i < NPL; ++i) {
+    const int j = lane + 64 * i;
+    float v = j < m ? s[j] : 0.f;
+    v = v > 0.f ? (v < 1.f ? v : 1.f) : 0.f;  // NaN -> 0
+    u[i] = (uint64_t)floor((double)v * 4294967296.0);
+    tl += u[i];
+  }
+  const uint64_t T = wave_sum_u64(tl);
+  if (T == 0) {  // every candidate has zero mass: the first in (u desc, j asc) order is j = 0
+    if (lane == 0) {
+      out[0] = 0;
+      cnt[row] = 1;
+    }
+    return;
+  }
+  const double prod = (double)tau * (double)T;
+  const uint64_t target = (uint64_t)ceil(prod);
+
+  // largest v in [0, 2^32] with F(v) >= target; F(0) = T >= target, F(2^32 + 1) = 0
+  uint64_t lo = 0, hi = (1ull << 32) + 1;
+  while (hi - lo > 1) {
+    const uint64_t mid = (lo + hi) >> 1;
+    uint64_t f = 0;
+#pragma unroll
+    for (int i = 0; i < NPL; ++i) f += u[i] >= mid ? u[i] : 0;
+    if (wave_sum_u64(f) >= target) lo = mid;
+    else hi = mid;
+  }
+  const uint64_t vstar = lo;  // >= 1 because F(1) = T >= target
+  uint64_t bl = 0;
+#pragma unroll
+  for (int i = 0; i < NPL; ++i) bl += u[i] > vstar ? u[i] : 0;
+  const uint64_t base = wave_sum_u64(bl);  // < target by maximality of v*
+  const uint64_t ties_needed = (target - base + vstar - 1) / vstar;
+
+  const uint64_t below = (1ull << lane) - 1ull;
+  uint32_t written = 0;
+  uint64_t ties_seen = 0;
+#pragma unroll
+  for (int i = 0; i < NPL; ++i) {
+    const int j = lane + 64 * i;
+    const bool tie = (j < m) && (u[i] == vstar);
+    const uint64_t tmask = __ballot(tie);
+    const uint64_t rank = ties_seen + (uint64_t)__popcll(tmask & below);
+    const bool sel = (j < m) && (u[i] > vstar || (tie && rank < ties_needed));
+    const uint64_t smask = __ballot(sel);
+    if (sel) out[written + __popcll(smask & below)] = j;
+    written += __popcll(smask);
+    ties_seen += __popcll(tmask);
+  }
+  if (lane == 0) cnt[row] = (int32_t)written;
+}
+
+template <int NPL>
+hipError_t launch_npl(const float* scores, const XattnShape& s, float tau, int32_t* idx,
+                      int32_t* cnt, hipStream_t st) {
+  const int n_rows = s.HQ() * s.NB();
+  const dim3 grid((n_rows + 3) / 4);
+  if (s.causal)
+    hipLaunchKernelGGL((select_kernel<NPL, true>), grid, dim3(256), 0, st, scores, n_rows,
+                       s.NB(), tau, idx, cnt);
+  else
+    hipLaunchKernelGGL((select_kernel<NPL, false>), grid, dim3(256), 0, st, scores, n_rows,
+                       s.NB(), tau, idx, cnt);
+  return hipGetLastError();
+}
+
+}  // namespace
+
+hipError_t launch_select(const float* scores, const XattnShape& s, float tau, int32_t* idx,
+                         int32_t* cnt, hipStream_t st) {
+  const int NB = s.NB();
+  if (NB <= 64) return launch_npl<1>(scores, s, tau, idx, cnt, st);
+  if (NB <= 128) return launch_npl<2>(scores, s, tau, idx, cnt, st);
+  if (NB <= 256) return launch_npl<4>(scores, s, tau, idx, cnt, st);
+  if (NB <= 512) return launch_npl<8>(scores, s, tau, idx, cnt, st);
+  if (NB <= 1024) return launch_npl<16>(scores, s, tau, idx, cnt, st);
+  if (NB <= 2048) return launch_npl<32>(scores, s, tau, idx, cnt, st);
+  return hipErrorInvalidValue;
+}

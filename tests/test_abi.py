@@ -1,0 +1,113 @@
+"""C ABI checks that need no GPU: the library loads, exports every entry point
+include/xattn.h declares, and rejects bad arguments on the host before any
+HIP call is made."""
+import ctypes
+import os
+import re
+
+import pytest
+
+import paper_2503_16428_amd as X
+from paper_2503_16428_amd import binding as B
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "xattn.h")
+
+
+def declared_functions():
+    src = open(HEADER).read()
+    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+    return sorted(set(re.findall(r"\b(xattn_[a-z_0-9]+)\s*\(", src)))
+
+
+def test_header_and_binding_agree():
+    decl = declared_functions()
+    assert "xattn_score" in decl and "xattn_block_sparse_attn" in decl
+    assert sorted(B.EXPORTS) == decl
+
+
+def test_library_exports_every_declared_symbol():
+    L = ctypes.CDLL(X.lib_path())
+    for name in declared_functions():
+        assert hasattr(L, name), name
+    assert X.version() == 100
+
+
+def test_nm_shows_exports():
+    import subprocess
+    out = subprocess.run(["nm", "-D", "--defined-only", X.lib_path()], capture_output=True,
+                         text=True, check=True).stdout
+    syms = set(re.findall(r"\bT (xattn_\w+)", out))
+    assert set(declared_functions()) <= syms
+
+
+def _dims(**kw):
+    d = dict(batch=1, hq=4, hkv=2, seq=1024, head_dim=128, causal=1)
+    d.update(kw)
+    return B.Dims(**d)
+
+
+def _score_ws(d, block=128, stride=8):
+    n = ctypes.c_size_t(0)
+    rc = X.lib().xattn_score_workspace_size(ctypes.byref(d), block, stride, ctypes.byref(n))
+    return rc, n.value
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(seq=1000), B.XATTN_ERR_ARG),
+    (dict(hq=3, hkv=2), B.XATTN_ERR_ARG),
+    (dict(hkv=0), B.XATTN_ERR_ARG),
+    (dict(batch=0), B.XATTN_ERR_ARG),
+    (dict(causal=2), B.XATTN_ERR_ARG),
+    (dict(head_dim=64), B.XATTN_ERR_UNSUPPORTED),
+    (dict(seq=128 * 2049), B.XATTN_ERR_UNSUPPORTED),
+])
+def test_bad_dims_are_rejected(kw, code):
+    rc, _ = _score_ws(_dims(**kw))
+    assert rc == code
+    assert X.lib().xattn_last_error().decode()
+
+
+@pytest.mark.parametrize("block,stride,code", [
+    (64, 8, B.XATTN_ERR_UNSUPPORTED), (0, 8, B.XATTN_ERR_ARG), (128, 3, B.XATTN_ERR_ARG),
+    (128, 0, B.XATTN_ERR_ARG), (128, 128, B.XATTN_ERR_UNSUPPORTED), (128, 256, B.XATTN_ERR_ARG),
+])
+def test_bad_block_or_stride(block, stride, code):
+    rc, _ = _score_ws(_dims(), block, stride)
+    assert rc == code
+
+
+def test_workspace_sizes_cover_partials():
+    d = _dims(hq=32, hkv=8, seq=131072)
+    rc, n = _score_ws(d, 128, 16)
+    assert rc == 0
+    NR, NB = 131072 // 16, 1024
+    assert n >= 32 * NR * NB * 4
+    lay = B.forward_layout(d, 128, 16)
+    assert lay["scores"] == 0 and lay["idx"] >= 32 * NB * NB * 4
+    assert all(v % 256 == 0 for v in lay.values())
+    assert B.forward_workspace_size(d, 128, 16) == lay["scratch"] + n
+
+
+def test_calls_validate_before_launch():
+    L = X.lib()
+    d = _dims()
+    fake = ctypes.c_void_p(0x1000)   # never dereferenced: every case fails validation
+    assert L.xattn_score(None, fake, ctypes.byref(d), 128, 8, fake, fake, 1 << 40, None) == \
+        B.XATTN_ERR_ARG
+    assert L.xattn_score(fake, fake, ctypes.byref(d), 128, 8, fake, None, 0, None) == \
+        B.XATTN_ERR_WORKSPACE
+    assert L.xattn_score(fake, fake, ctypes.byref(d), 128, 8, fake, fake, 16, None) == \
+        B.XATTN_ERR_WORKSPACE
+    for tau in (0.0, -1.0, float("nan")):
+        assert L.xattn_select(fake, ctypes.byref(d), 128, tau, fake, fake, None) == \
+            B.XATTN_ERR_ARG
+    assert L.xattn_select(None, ctypes.byref(d), 128, 0.9, fake, fake, None) == B.XATTN_ERR_ARG
+    assert L.xattn_block_sparse_attn(fake, fake, fake, ctypes.byref(d), 128, None, fake, fake,
+                                     None, None) == B.XATTN_ERR_ARG
+    assert L.xattn_dense_attn(fake, fake, None, ctypes.byref(d), fake, None, None) == \
+        B.XATTN_ERR_ARG
+    assert L.xattn_forward(fake, fake, fake, ctypes.byref(d), 128, 8, 0.9, fake, None, fake, 8,
+                           None) == B.XATTN_ERR_WORKSPACE
+    assert L.xattn_dense_attn(fake, fake, fake, None, fake, None, None) == B.XATTN_ERR_ARG
+    assert L.xattn_strerror(99) == b"unknown status"

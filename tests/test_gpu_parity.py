@@ -1,0 +1,211 @@
+"""GPU parity: every kernel against the fp64 CPU oracle on the same seeded
+inputs, through the C ABI (thin ctypes binding). Small sizes that span
+several tiles and a ragged tail; full-size sampled rows live in
+test_gpu_full.py."""
+import numpy as np
+import pytest
+
+import oracle
+import workloads as W
+
+from .helpers import (OUT_MAX_ABS, OUT_MEAN_ABS, compare_index_sets, compare_scores,
+                      dev_bf16, host_f32, logit_error_bound, score_tolerance)
+
+pytestmark = pytest.mark.gpu
+
+torch = pytest.importorskip("torch")
+if not torch.cuda.is_available():
+    pytest.skip("no GPU", allow_module_level=True)
+
+import paper_2503_16428_amd as X  # noqa: E402
+
+
+def _inputs(L, hq, hkv, seed, kind="clustered"):
+    w = W.small("t", L, hq=hq, hkv=hkv, seed=seed, kind=kind)
+    return W.generate(w)
+
+
+def _attn_err(o_gpu, o_ref):
+    e = np.abs(o_gpu.astype(np.float64) - o_ref)
+    return float(e.max()), float(e.mean())
+
+
+@pytest.mark.parametrize("causal", [True, False])
+def test_dense_attention_matches_oracle(causal):
+    L, hq, hkv = 640, 4, 2
+    x = _inputs(L, hq, hkv, seed=101)
+    q, k, v = (dev_bf16(x[n]) for n in "qkv")
+    print(f"dense attn L={L} hq={hq} hkv={hkv} causal={causal}", flush=True)
+    o, lse = X.xattn_dense_attn(q, k, v, causal=causal)
+    torch.cuda.synchronize()
+    o_ref, lse_ref = oracle.dense_attn_rows(x["q"], x["k"], x["v"], 128, causal)
+    mx, mean = _attn_err(host_f32(o).reshape(o_ref.shape), o_ref)
+    print(f"  max_abs={mx:.3e} mean_abs={mean:.3e}")
+    assert mx <= OUT_MAX_ABS and mean <= OUT_MEAN_ABS
+    np.testing.assert_allclose(host_f32(lse).reshape(lse_ref.shape), lse_ref, rtol=2e-3, atol=2e-2)
+
+
+@pytest.mark.parametrize("causal", [True, False])
+def test_sparse_attention_on_generated_lists(causal):
+    L, hq, hkv = 1280, 4, 1
+    NB = L // 128
+    x = _inputs(L, hq, hkv, seed=102)
+    rng = np.random.default_rng(7)
+    idx = np.full((hq * NB, NB), -1, np.int32)
+    cnt = np.zeros(hq * NB, np.int32)
+    for r in range(hq * NB):
+        b = r % NB
+        cand = np.arange(b + 1) if causal else np.arange(NB)
+        n = rng.integers(0, len(cand) + 1)          # includes empty lists
+        sel = np.sort(rng.choice(cand, n, replace=False))
+        idx[r, :n] = sel
+        cnt[r] = n
+    q, k, v = (dev_bf16(x[n]) for n in "qkv")
+    di = torch.from_numpy(idx.reshape(hq, NB, NB)).cuda()
+    dc = torch.from_numpy(cnt.reshape(hq, NB)).cuda()
+    print(f"sparse attn generated lists L={L} causal={causal}", flush=True)
+    o, lse = X.xattn_block_sparse_attn(q, k, v, di, dc, causal=causal)
+    torch.cuda.synchronize()
+    o_ref, lse_ref = oracle.sparse_attn_rows(x["q"], x["k"], x["v"], 128, idx, cnt, causal)
+    og = host_f32(o).reshape(o_ref.shape)
+    lg = host_f32(lse).reshape(lse_ref.shape)
+    empty = ~np.isfinite(lse_ref)
+    assert np.all(og[empty] == 0) and np.all(np.isneginf(lg[empty]))
+    mx, mean = _attn_err(og[~empty], o_ref[~empty])
+    print(f"  max_abs={mx:.3e} mean_abs={mean:.3e} empty_queries={int(empty.sum())}")
+    assert mx <= OUT_MAX_ABS and mean <= OUT_MEAN_ABS
+    np.testing.assert_allclose(lg[~empty], lse_ref[~empty], rtol=2e-3, atol=2e-2)
+
+
+@pytest.mark.parametrize("causal", [True, False])
+def test_dense_is_bitwise_sparse_with_full_lists(causal):
+    L, hq, hkv = 768, 2, 1
+    NB = L // 128
+    x = _inputs(L, hq, hkv, seed=103)
+    q, k, v = (dev_bf16(x[n]) for n in "qkv")
+    idx = np.full((hq, NB, NB), -1, np.int32)
+    cnt = np.zeros((hq, NB), np.int32)
+    for b in range(NB):
+        m = b + 1 if causal else NB
+        idx[:, b, :m] = np.arange(m)
+        cnt[:, b] = m
+    o1, l1 = X.xattn_dense_attn(q, k, v, causal=causal)
+    o2, l2 = X.xattn_block_sparse_attn(q, k, v, torch.from_numpy(idx).cuda(),
+                                       torch.from_numpy(cnt).cuda(), causal=causal)
+    torch.cuda.synchronize()
+    assert torch.equal(o1.view(torch.int16), o2.view(torch.int16))
+    assert torch.equal(l1, l2)
+
+
+@pytest.mark.parametrize("S", [1, 2, 4, 8, 16, 32, 64])
+@pytest.mark.parametrize("causal", [True, False])
+def test_scores_match_oracle(S, causal):
+    L = 128 * 37 if S > 1 else 128 * 21      # ragged reduced tiles for S >= 2
+    hq, hkv = 2, 1
+    x = _inputs(L, hq, hkv, seed=200 + S)
+    q, k = dev_bf16(x["q"]), dev_bf16(x["k"])
+    print(f"score S={S} L={L} causal={causal}", flush=True)
+    sc = X.xattn_score(q, k, causal=causal, stride=S)
+    torch.cuda.synchronize()
+    NB = L // 128
+    want = oracle.score_rows(x["q"], x["k"], 128, S, causal)
+    got = host_f32(sc).reshape(want.shape)
+    rh, rb = oracle.all_rows(hq, NB)
+    sel = np.arange(0, len(rh), 5)
+    dz = logit_error_bound(x["q"], x["k"], S, rh[sel], rb[sel], hq // hkv)
+    rep = compare_scores(got, want, dz)
+    print(f"  {rep}")
+    assert rep["n_bad"] == 0
+    if causal:
+        assert np.all(got[np.triu(np.ones((NB, NB), bool), 1)[rb]] == 0)
+    np.testing.assert_allclose(got.sum(-1), 1.0, atol=1e-4)
+
+
+@pytest.mark.parametrize("causal", [True, False])
+@pytest.mark.parametrize("NB", [5, 64, 65, 300, 1024, 2048])
+def test_select_is_bit_exact_on_same_scores(NB, causal):
+    rows = 64 if NB >= 1024 else 200
+    s, rb = W.random_score_rows(rows, NB, seed=NB, causal=causal)
+    s2, _ = W.random_score_rows(rows, NB, seed=NB + 1, causal=causal, ties=True)
+    H = 2
+    # a score tensor [H][NB][NB] whose row (h, b) is one generated row
+    full = np.zeros((H, NB, NB), np.float32)
+    for r in range(rows):
+        h, b = r % H, (int(rb[r]) if causal else r % NB)
+        full[h, b] = (s if r % 2 == 0 else s2)[r]
+    dims = X.Dims(1, H, 1, NB * 128, 128, int(causal))
+    for tau in (0.5, 0.8, 0.9, 0.95, 1.0):
+        print(f"select NB={NB} causal={causal} tau={tau}", flush=True)
+        idx, cnt = X.xattn_select(torch.from_numpy(full).cuda(), dims, tau)
+        torch.cuda.synchronize()
+        idx, cnt = idx.cpu().numpy(), cnt.cpu().numpy()
+        flat = full.reshape(H * NB, NB).astype(np.float64)
+        allb = np.tile(np.arange(NB, dtype=np.int32), H)
+        oi, oc = oracle.select_rows(flat, allb, tau, causal)
+        gc = cnt.reshape(-1)
+        gi = idx.reshape(H * NB, NB)
+        assert np.array_equal(gc, oc)
+        for r in range(H * NB):
+            assert np.array_equal(gi[r, :gc[r]], oi[r, :oc[r]]), (r, tau)
+
+
+def test_select_on_oracle_scores_rounded_to_fp32():
+    L, hq, hkv, S = 2048, 4, 2, 8
+    x = _inputs(L, hq, hkv, seed=301)
+    NB = L // 128
+    sc = oracle.score_rows(x["q"], x["k"], 128, S, True).astype(np.float32)
+    dims = X.Dims(1, hq, hkv, L, 128, 1)
+    idx, cnt = X.xattn_select(torch.from_numpy(sc.reshape(hq, NB, NB)).cuda(), dims, 0.9)
+    torch.cuda.synchronize()
+    _, rb = oracle.all_rows(hq, NB)
+    oi, oc = oracle.select_rows(sc.astype(np.float64), rb, 0.9, True)
+    gi, gc = idx.cpu().numpy().reshape(hq * NB, NB), cnt.cpu().numpy().reshape(-1)
+    assert np.array_equal(gc, oc)
+    for r in range(hq * NB):
+        assert np.array_equal(gi[r, :gc[r]], oi[r, :oc[r]])
+
+
+@pytest.mark.parametrize("causal,S,kind", [(True, 8, "clustered"), (True, 16, "clustered_local"),
+                                           (False, 16, "clustered")])
+def test_forward_end_to_end_small(causal, S, kind):
+    L, hq, hkv, tau = 3072, 4, 2, 0.9
+    x = _inputs(L, hq, hkv, seed=401, kind=kind)
+    NB = L // 128
+    q, k, v = (dev_bf16(x[n]) for n in "qkv")
+    print(f"forward L={L} S={S} causal={causal} kind={kind}", flush=True)
+    o, _, views = X.xattn_forward(q, k, v, causal=causal, stride=S, tau=tau)
+    torch.cuda.synchronize()
+    f = oracle.forward_rows(x["q"], x["k"], x["v"], 128, S, tau, causal)
+    rh, rb = oracle.all_rows(hq, NB)
+    dz = logit_error_bound(x["q"], x["k"], S, rh[::7], rb[::7], hq // hkv)
+    rep = compare_scores(host_f32(views["scores"]).reshape(f["scores"].shape), f["scores"], dz)
+    print(f"  scores {rep}")
+    assert rep["n_bad"] == 0
+    gi = views["idx"].cpu().numpy().reshape(hq * NB, NB)
+    gc = views["cnt"].cpu().numpy().reshape(-1)
+    n_eq, n_margin, n_tie, bad = compare_index_sets(gi, gc, f["idx"], f["cnt"], f["scores"], rb,
+                                                    tau, causal, score_tolerance(dz)[0])
+    dens = gc.sum() / (np.arange(1, NB + 1).sum() * hq if causal else NB * NB * hq)
+    print(f"  index rows: equal={n_eq} margin={n_margin} tie={n_tie} bad={len(bad)} "
+          f"density={dens:.3f}")
+    assert not bad, bad[:5]
+    og = host_f32(o).reshape(f["o"].shape)
+    same = np.array([np.array_equal(gi[r, :gc[r]], f["idx"][r, :f["cnt"][r]])
+                     for r in range(hq * NB)])
+    mx, mean = _attn_err(og[same], f["o"][same])
+    print(f"  output on {same.sum()} identical-list rows: max_abs={mx:.3e} mean_abs={mean:.3e}")
+    assert mx <= OUT_MAX_ABS and mean <= OUT_MEAN_ABS
+
+
+def test_repeated_calls_are_bitwise_deterministic():
+    L, hq, hkv = 2048, 4, 2
+    x = _inputs(L, hq, hkv, seed=501)
+    q, k, v = (dev_bf16(x[n]) for n in "qkv")
+    outs = []
+    for _ in range(2):
+        o, lse, views = X.xattn_forward(q, k, v, causal=True, stride=8, tau=0.9, want_lse=True)
+        torch.cuda.synchronize()
+        outs.append((o.clone(), lse.clone(), views["scores"].clone(), views["cnt"].clone()))
+    for a, b in zip(*outs):
+        assert torch.equal(a.view(torch.uint8) if a.dtype == torch.bfloat16 else a,
+                           b.view(torch.uint8) if b.dtype == torch.bfloat16 else b)
