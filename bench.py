@@ -1,0 +1,252 @@
+#!/usr/bin/env python3
+"""Benchmark of the XAttention prefill path on one MI355X.
+
+One step = one full pass of the hot path over one layer of synthetic input:
+antidiagonal scoring -> threshold selection -> block-sparse attention, all
+heads. Default workload: 128K tokens, 32 query / 8 KV heads (GQA), head_dim
+128, causal, B = 128, S = 16, tau = 0.9, clustered Q/K with a local key bias.
+
+Prints ONE JSON line: ms per layer and dense-equivalent TFLOP/s (the value),
+per-stage times, density, speedup over the library's own dense mode, the
+roofline of the dominant kernel and the CPU oracle baseline on a sample.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import math
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+import numpy as np  # noqa: E402
+
+import workloads as W  # noqa: E402
+
+PEAK_BF16_TFLOPS = 2500.0      # MI355X dense bf16 MFMA
+PEAK_HBM_GBS = 8000.0
+
+
+def parse():
+    ap = argparse.ArgumentParser(description=__doc__.splitlines()[0])
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--workload", default="c3", choices=sorted(W.WORKLOADS))
+    ap.add_argument("--stride", type=int, default=None)
+    ap.add_argument("--tau", type=float, default=None)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-dense", action="store_true")
+    ap.add_argument("--dense-steps", type=int, default=3)
+    ap.add_argument("--copy-calibration", action="store_true",
+                    help="after the timed region, copy a 256 MiB buffer once (a plain copy "
+                         "kernel of known size, to scale rocprofv3 FETCH_SIZE/WRITE_SIZE)")
+    ap.add_argument("--cpu-rows", type=int, default=2048,
+                    help="query-block rows the CPU oracle computes for the baseline")
+    ap.add_argument("--traffic-file", default=os.path.join(ROOT, "profiles", "hbm_traffic.txt"),
+                    help="HBM bytes per launch measured by rocprofv3 --pmc (if present)")
+    return ap.parse_args()
+
+
+def dev_bf16(u16):
+    """uint16 bf16 bit patterns (host) -> torch bf16 device tensor."""
+    import torch
+    return torch.from_numpy(np.ascontiguousarray(u16).view(np.int16)).view(torch.bfloat16).cuda()
+
+
+def dense_flops(w) -> float:
+    """4 L^2 d per head (QK^T and PV), halved when causal (diagonal halves)."""
+    f = 4.0 * w.seq * w.seq * w.head_dim * w.hq * w.batch
+    return f / 2 if w.causal else f
+
+
+def cpu_baseline(w, x, n_rows: int):
+    """The CPU oracle (fp64, OpenMP) on a bounded sample of query-block rows:
+    score + select + sparse attention for those rows, reported as dense-
+    equivalent TFLOP/s of the rows it processed."""
+    import oracle
+    NB = w.n_blocks
+    rng = np.random.default_rng(12345)
+    heads = rng.integers(0, w.hq * w.batch, n_rows).astype(np.int32)
+    blocks = np.linspace(0, NB - 1, n_rows).round().astype(np.int32)
+    t0 = time.perf_counter()
+    f = oracle.forward_rows(x["q"], x["k"], x["v"], w.block, w.stride, w.tau, w.causal,
+                            rows=(heads, blocks))
+    dt = time.perf_counter() - t0
+    kv = (blocks.astype(np.float64) + 1) if w.causal else np.full(n_rows, NB, np.float64)
+    flops = float((4.0 * w.block * w.block * w.head_dim * kv).sum())
+    if w.causal:
+        flops -= 4.0 * w.block * w.block * w.head_dim * n_rows / 2   # half diagonal
+    return {
+        "value": flops / dt / 1e12, "unit": "TFLOP/s (dense-equivalent)",
+        "cores": oracle.num_threads(), "kind": "oracle",
+        "sample": f"{n_rows} query-block rows (random heads, blocks spread over 0..{NB - 1}) "
+                  f"of the same layer: score+select+sparse attention in fp64, {dt:.1f} s",
+        "seconds": dt, "rows_density": float(f["cnt"].sum() / kv.sum()),
+    }
+
+
+def read_traffic(path, w, kernel):
+    """HBM bytes per launch (FETCH_SIZE + WRITE_SIZE, calibrated against a copy
+    kernel) from the profile summary: lines 'workload kernel stride tau bytes'.
+    None if absent or taken for another configuration."""
+    if not os.path.exists(path):
+        return None
+    for line in open(path):
+        f = line.split()
+        if len(f) == 5 and not line.startswith("#") and f[0] == w.name and f[1] == kernel \
+                and int(f[2]) == w.stride and abs(float(f[3]) - w.tau) < 1e-9:
+            return float(f[4])
+    return None
+
+
+def main():
+    a = parse()
+    if a.gpus != 1:
+        print(json.dumps({"error": "this build runs on exactly one GPU; multi-GPU runs are "
+                                   "not part of it (--gpus must be 1)"}), flush=True)
+        sys.exit(2)
+    import torch
+    import paper_2503_16428_amd as X
+
+    w = W.WORKLOADS[a.workload]
+    if a.stride is not None:
+        w = w.with_(stride=a.stride)
+    if a.tau is not None:
+        w = w.with_(tau=a.tau)
+    NB = w.n_blocks
+    t0 = time.perf_counter()
+    x = W.generate(w, threads=16)
+    gen_s = time.perf_counter() - t0
+    print(f"# generated {w.name} in {gen_s:.1f} s", file=sys.stderr, flush=True)
+    q, k, v = (dev_bf16(x[n]) for n in "qkv")
+    dev = q.device
+    dims = X.make_dims(q, k, w.causal)
+    scores = torch.empty((dims.heads, NB, NB), dtype=torch.float32, device=dev)
+    idx = torch.empty((dims.heads, NB, NB), dtype=torch.int32, device=dev)
+    cnt = torch.empty((dims.heads, NB), dtype=torch.int32, device=dev)
+    o = torch.empty_like(q)
+    ws = torch.empty(X.score_workspace_size(dims, w.block, w.stride), dtype=torch.uint8,
+                     device=dev)
+    stream = torch.cuda.current_stream()
+
+    def step(ev=None):
+        if ev is not None:
+            ev[0].record(stream)
+        X.xattn_score(q, k, w.causal, w.block, w.stride, scores=scores, workspace=ws)
+        if ev is not None:
+            ev[1].record(stream)
+        X.xattn_select(scores, dims, w.tau, w.block, idx=idx, cnt=cnt)
+        if ev is not None:
+            ev[2].record(stream)
+        X.xattn_block_sparse_attn(q, k, v, idx, cnt, w.causal, w.block, o=o, want_lse=False)
+        if ev is not None:
+            ev[3].record(stream)
+
+    for _ in range(a.warmup):
+        step()
+    torch.cuda.synchronize()
+    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(a.steps)]
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for i in range(a.steps):
+        step(evs[i])
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    print(f"# timed {a.steps} steps in {wall:.2f} s", file=sys.stderr, flush=True)
+    st = np.array([[e[0].elapsed_time(e[1]), e[1].elapsed_time(e[2]), e[2].elapsed_time(e[3])]
+                   for e in evs])
+    ms_step = wall * 1e3 / a.steps
+    t_score, t_select, t_attn = (float(v) for v in st.mean(0))
+
+    c = cnt.cpu().numpy().astype(np.int64)
+    cand = (np.arange(1, NB + 1) if w.causal else np.full(NB, NB)) * dims.heads
+    density = float(c.sum() / cand.sum())
+    computed_blocks = int(c.sum())
+    attn_flops = computed_blocks * 4.0 * w.block * w.block * w.head_dim
+    dflops = dense_flops(w)
+    stage_sum = t_score + t_select + t_attn
+
+    if a.copy_calibration:
+        src = torch.ones(256 << 20, dtype=torch.uint8, device=dev)
+        dst = torch.empty_like(src)
+        torch.cuda.synchronize()
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        del src, dst
+
+    dense_ms = None
+    if not a.no_dense:
+        X.xattn_dense_attn(q, k, v, w.causal, o=o, want_lse=False)
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        for _ in range(a.dense_steps):
+            X.xattn_dense_attn(q, k, v, w.causal, o=o, want_lse=False)
+        e1.record(stream)
+        torch.cuda.synchronize()
+        dense_ms = e0.elapsed_time(e1) / a.dense_steps
+        print(f"# dense mode {dense_ms:.2f} ms", file=sys.stderr, flush=True)
+
+    # dominant kernel of the step and its roofline (algorithmic FLOPs per launch)
+    NR = w.seq // w.stride
+    score_flops = 2.0 * NR * NR * w.stride * w.head_dim * dims.heads
+    if w.causal:
+        score_flops /= 2
+    kernels = {
+        "attn": {"ms": t_attn, "flops": attn_flops},
+        "score": {"ms": t_score, "flops": score_flops},
+    }
+    dom = max(kernels, key=lambda n: kernels[n]["ms"])
+    ach = kernels[dom]["flops"] / (kernels[dom]["ms"] * 1e-3) / 1e12
+    traffic = read_traffic(a.traffic_file, w, dom)
+    roofline = {"bound": "mfma", "kernel": dom, "achieved": round(ach, 2),
+                "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s", "frac": round(ach / PEAK_BF16_TFLOPS, 4),
+                "traffic": traffic,
+                "per_launch_flops": kernels[dom]["flops"],
+                "avg_launch_ms": round(kernels[dom]["ms"], 4),
+                "flops_convention": ("computed 128x128 blocks x 4*B^2*d (diagonal blocks in "
+                                     "full)" if dom == "attn" else
+                                     "2 * (L/S)^2 * S*d per head, halved when causal")}
+
+    cpu = None
+    if not a.no_cpu_baseline:
+        print("# cpu baseline (oracle) ...", file=sys.stderr, flush=True)
+        cpu = cpu_baseline(w, x, a.cpu_rows)
+        cpu["seconds"] = round(cpu["seconds"], 2)
+        cpu["value"] = round(cpu["value"], 6)
+
+    value = dflops / (ms_step * 1e-3) / 1e12
+    out = {
+        "metric": "ms/layer + dense-equiv TFLOP/s of scored block-sparse prefill at 128K",
+        "value": round(value, 3),
+        "unit": "TFLOP/s (dense-equivalent)",
+        "n_gpus": 1, "steps": a.steps, "warmup": a.warmup,
+        "ms_per_step": round(ms_step, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic",
+        "config": w.describe(),
+        "stages_ms": {"score": round(t_score, 4), "select": round(t_select, 4),
+                      "attn": round(t_attn, 4)},
+        "score_select_share": round((t_score + t_select) / stage_sum, 4),
+        "density": round(density, 5),
+        "dense_ms": None if dense_ms is None else round(dense_ms, 3),
+        "speedup_vs_dense": None if dense_ms is None else round(dense_ms / ms_step, 3),
+        "attn_mfma_frac_computed_blocks": round(attn_flops / (t_attn * 1e-3) / 1e12 /
+                                                PEAK_BF16_TFLOPS, 4),
+        "score_mfma_frac": round(score_flops / (t_score * 1e-3) / 1e12 / PEAK_BF16_TFLOPS, 4),
+        "roofline": roofline,
+        "cpu_baseline": cpu,
+    }
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()
