@@ -38,38 +38,30 @@ __device__ __forceinline__ uint32_t cvt_pk_bf16(float a, float b) {
   return __builtin_bit_cast(uint32_t, __builtin_convertvector(f32v2{a, b}, bf16v2));
 }
 
-// Workgroup barrier without a memory fence. Ordering of the LDS tiles is
-// explicit: each wave waits (vmcnt) for its own direct-to-LDS loads before
-// the barrier, and every LDS read has been consumed before the barrier that
-// lets the buffer be refilled. (__syncthreads would also wait for the
-// prefetch that is meant to stay in flight.)
-__device__ __forceinline__ void barrier_nofence() { asm volatile("s_barrier" ::: "memory"); }
-
-// Element offset of logical 16-byte chunk c of row r in a swizzled [128][128] tile.
-__device__ __forceinline__ int swz(int r, int c) { return r * kHeadDim + ((c ^ (r & 15)) << 3); }
-
-// This wave's share of one 128 x 128 bf16 tile: 8 x (4 rows x 256 B).
-// Direct-to-LDS load of 16 bytes per lane: lane l's bytes land at LDS byte
-// address lds + 16 l (lds wave-uniform, through M0). Issued as inline asm so
-// the compiler does not track it: without alias information it would stall
-// every LDS read on every load in flight. The kernel orders these loads
-// itself (explicit vmcnt waits + barriers).
-__device__ __forceinline__ void dma16(const uint16_t* sbase, uint32_t voff, uint32_t lds) {
-  asm volatile("s_mov_b32 m0, %2\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, %1"
-               :
-               : "v"(voff), "s"(sbase), "s"(lds)
-               : "memory", "m0");
+// Element offset of logical 16-byte chunk c of row r in a swizzled [128][128]
+// tile. K tiles are read 16 rows at one chunk (ds_read_b128): chunk ^ (r mod 16)
+// spreads them over 16 bank groups. V tiles are read as 4-row x 32-byte
+// patches (ds_read_b64_tr_b16): chunk ^ (4 (r mod 4) | (r / 4) mod 4) puts the
+// 8 row/chunk pairs of a patch, and of two patches side by side, on distinct
+// bank groups.
+__device__ __forceinline__ int swz_k(int r, int c) { return r * kHeadDim + ((c ^ (r & 15)) << 3); }
+__device__ __forceinline__ int swz_v_mask(int r) { return ((r & 3) << 2) | ((r >> 2) & 3); }
+__device__ __forceinline__ int swz_v(int r, int c) {
+  return r * kHeadDim + ((c ^ swz_v_mask(r)) << 3);
 }
 
+// This wave's share of one 128 x 128 bf16 tile: 8 x (4 rows x 256 B).
 // Per-lane byte offsets of this wave's 8 loads of a 128 x 128 bf16 tile: load
-// i covers rows 4i .. 4i+3 of the wave's 32 rows; rows 16 apart share the
-// swizzle, so loads i and i+4 use the same offset (+4 KB on the scalar base).
+// i covers rows 4i .. 4i+3 of the wave's 32 rows, lane l filling physical
+// chunk l mod 16 of row 4i + l / 16. Rows 16 apart share the swizzle (both
+// layouts), so loads i and i+4 use the same offset (+4 KB on the scalar base).
+template <bool VTILE>
 __device__ __forceinline__ void tile_offsets(int lane, uint32_t voff[4]) {
 #pragma unroll
   for (int i = 0; i < 4; ++i) {
-    const uint32_t r = (uint32_t)(4 * i + (lane >> 4));
-    const uint32_t c = (uint32_t)(lane & 15) ^ (r & 15u);
-    voff[i] = (r * kHeadDim + c * 8) * 2;
+    const int r = 4 * i + (lane >> 4);
+    const int c = (lane & 15) ^ (VTILE ? swz_v_mask(r) : (r & 15));
+    voff[i] = (uint32_t)((r * kHeadDim + c * 8) * 2);
   }
 }
 
@@ -139,13 +131,14 @@ __device__ __forceinline__ void attn_body(bool dense,
     return j < 0 ? 0 : (j >= NB ? NB - 1 : j);  // memory-safe on malformed lists
   };
 
-  uint32_t voff[4];
-  tile_offsets(lane, voff);
-  const uint32_t ks_lds = (uint32_t)(uintptr_t)LDS_PTR(Ks);
-  const uint32_t vs_lds = (uint32_t)(uintptr_t)LDS_PTR(Vs);
+  uint32_t koff[4], voff[4];
+  tile_offsets<false>(lane, koff);
+  tile_offsets<true>(lane, voff);
+  const uint32_t ks_lds = XATTN_LDS_ADDR(Ks);
+  const uint32_t vs_lds = XATTN_LDS_ADDR(Vs);
   int j = n_kb > 0 ? block_at(0) : 0;
   if (n_kb > 0) {
-    issue_tile(ks_lds, Kg + (size_t)j * kBlock * kHeadDim, wv, voff);
+    issue_tile(ks_lds, Kg + (size_t)j * kBlock * kHeadDim, wv, koff);
     issue_tile(vs_lds, Vg + (size_t)j * kBlock * kHeadDim, wv, voff);
   }
 
@@ -174,7 +167,7 @@ __device__ __forceinline__ void attn_body(bool dense,
     const int key0 = j * kBlock;
 
     // ---- K_j ready (V_j may still be in flight)
-    asm volatile("s_waitcnt vmcnt(8)" ::: "memory");
+    wait_vmcnt<8>();
     barrier_nofence();
     f32x16 sacc[4];
 #pragma unroll
@@ -182,7 +175,7 @@ __device__ __forceinline__ void attn_body(bool dense,
       sacc[kt] = f32x16{};
 #pragma unroll
       for (int s = 0; s < 8; ++s) {
-        const u32x4 a = *(const u32x4*)&Ks[swz(32 * kt + lr, 2 * s + lh)];
+        const u32x4 a = *(const u32x4*)&Ks[swz_k(32 * kt + lr, 2 * s + lh)];
         sacc[kt] = mfma32(as_bf16x8(a), qb[s], sacc[kt]);
       }
     }
@@ -193,7 +186,7 @@ __device__ __forceinline__ void attn_body(bool dense,
       __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // one MFMA
     }
     barrier_nofence();  // every wave is done with Ks
-    if constexpr (NEXT) issue_tile(ks_lds, Kg + (size_t)jn * kBlock * kHeadDim, wv, voff);
+    if constexpr (NEXT) issue_tile(ks_lds, Kg + (size_t)jn * kBlock * kHeadDim, wv, koff);
 
     // ---- online softmax (log2 domain); register r of tile kt is key
     // key0 + 32 kt + 8 (r/4) + 4 lh + r%4 of query qi
@@ -236,8 +229,8 @@ __device__ __forceinline__ void attn_body(bool dense,
     l_run += ls;
 
     // ---- V_j ready (K_jn may be in flight)
-    if constexpr (NEXT) asm volatile("s_waitcnt vmcnt(8)" ::: "memory");
-    else asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+    if constexpr (NEXT) wait_vmcnt<8>();
+    else wait_vmcnt<0>();
     barrier_nofence();
     // O^T += V_j^T P^T. MFMA step u covers keys 16u .. 16u+15; slot
     // 8 lh + jj of both operands is key 16u + 8 (jj/4) + 4 lh + jj%4.
@@ -252,9 +245,9 @@ __device__ __forceinline__ void attn_body(bool dense,
         const int c = 4 * dt + 2 * tg2 + ((tj & 3) >> 1);
         const int off = 4 * (tj & 1);
         const s16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
-            (__attribute__((address_space(3))) s16x4*)&Vs[swz(row, c) + off]);
+            (__attribute__((address_space(3))) s16x4*)&Vs[swz_v(row, c) + off]);
         const s16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
-            (__attribute__((address_space(3))) s16x4*)&Vs[swz(row + 8, c) + off]);
+            (__attribute__((address_space(3))) s16x4*)&Vs[swz_v(row + 8, c) + off]);
         const u32x2 lo2 = __builtin_bit_cast(u32x2, lo), hi2 = __builtin_bit_cast(u32x2, hi);
         oacc[dt] = mfma32(as_bf16x8(u32x4{lo2[0], lo2[1], hi2[0], hi2[1]}), pb, oacc[dt]);
       }

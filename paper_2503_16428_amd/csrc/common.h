@@ -38,6 +38,33 @@ __device__ __forceinline__ uint32_t pack_bf16x2(float a, float b) {
   return ua | ub;
 }
 
+// Direct-to-LDS load of 16 bytes per lane: lane l's bytes land at LDS byte
+// address lds + 16 l (lds wave-uniform, passed through M0); the global address
+// is sbase (scalar) + voff (per lane, bytes). Issued as inline asm so the
+// compiler does not track it: lacking alias information it would otherwise
+// stall every LDS read on every such load in flight. Kernels order these
+// loads themselves (explicit vmcnt waits + barriers).
+__device__ __forceinline__ void dma16(const void* sbase, uint32_t voff, uint32_t lds) {
+  asm volatile("s_mov_b32 m0, %2\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, %1"
+               :
+               : "v"(voff), "s"(sbase), "s"(lds)
+               : "memory", "m0");
+}
+
+// Wait until at most N of this wave's vector-memory loads are in flight.
+template <int N>
+__device__ __forceinline__ void wait_vmcnt() {
+  asm volatile("s_waitcnt vmcnt(%0)" ::"n"(N) : "memory");
+}
+
+// Workgroup barrier without a memory fence: LDS tiles are ordered explicitly
+// (each wave waits for its own direct-to-LDS loads before the barrier, and
+// every LDS read has been consumed before the barrier that frees a buffer);
+// __syncthreads would also wait for prefetches meant to stay in flight.
+__device__ __forceinline__ void barrier_nofence() { asm volatile("s_barrier" ::: "memory"); }
+
+#define XATTN_LDS_ADDR(p) ((uint32_t)(uintptr_t)((__attribute__((address_space(3))) void*)(p)))
+
 // Bijection blockIdx -> logical work index such that the workgroups one XCD
 // receives (blockIdx % 8 == x) cover one contiguous logical range; neighbours
 // in logical order then share that XCD's L2.
