@@ -28,6 +28,7 @@ using namespace xattn;
 namespace {
 
 constexpr int kThreads = 256;
+constexpr float kRescaleSlack = 8.f;  // log2 units: probabilities stay <= 256
 
 typedef __attribute__((__vector_size__(4 * sizeof(short)))) short s16x4;
 typedef __attribute__((ext_vector_type(2))) float f32v2;
@@ -154,7 +155,7 @@ __device__ __forceinline__ void attn_body(bool dense,
   f32x16 oacc[4];
 #pragma unroll
   for (int i = 0; i < 4; ++i) oacc[i] = f32x16{};
-  float m_run = -INFINITY, l_run = 0.f;
+  float m_ref = -INFINITY, l_run = 0.f;  // exponent reference (log2 domain), row sum
 
   // ds_read_b64_tr_b16 source addresses (see header): lane = (group G, index i)
   const int tj = lane & 15, tg2 = (lane >> 4) & 1;
@@ -189,30 +190,42 @@ __device__ __forceinline__ void attn_body(bool dense,
     if constexpr (NEXT) issue_tile(ks_lds, Kg + (size_t)jn * kBlock * kHeadDim, wv, koff);
 
     // ---- online softmax (log2 domain); register r of tile kt is key
-    // key0 + 32 kt + 8 (r/4) + 4 lh + r%4 of query qi
-    const bool mask = CAUSAL && (j >= b);
-    float mt = -INFINITY;
+    // key0 + 32 kt + 8 (r/4) + 4 lh + r%4 of query qi. Only blocks j >= b (the
+    // diagonal) need the causal mask; the empty asm keeps the compiler from
+    // turning this uniform branch into selects executed on every block.
+    if (CAUSAL && j >= b) {
+      asm volatile("");
+#pragma unroll
+      for (int kt = 0; kt < 4; ++kt) {
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          const int key = key0 + 32 * kt + 8 * (r >> 2) + 4 * lh + (r & 3);
+          if (key > qi) sacc[kt][r] = -INFINITY;
+        }
+      }
+    }
+    float mraw = -INFINITY;
 #pragma unroll
     for (int kt = 0; kt < 4; ++kt) {
 #pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        float x = sacc[kt][r] * scale_log2;
-        if (mask) {
-          const int key = key0 + 32 * kt + 8 * (r >> 2) + 4 * lh + (r & 3);
-          if (key > qi) x = -INFINITY;
-        }
-        sacc[kt][r] = x;
-        mt = fmaxf(mt, x);
-      }
+      for (int r = 0; r < 16; ++r) mraw = fmaxf(mraw, sacc[kt][r]);
     }
-    mt = fmaxf(mt, __shfl_xor(mt, 32));
-    const float m_new = fmaxf(m_run, mt);
-    const float m_use = (m_new == -INFINITY) ? 0.f : m_new;
-    const float alpha = fast_exp2(m_run - m_use);
-    m_run = m_new;
-    l_run *= alpha;
+    mraw = fmaxf(mraw, __shfl_xor(mraw, 32));
+    const float mt = mraw * scale_log2;  // scale > 0: max commutes with it
+    // Lazy rescaling: the exponent reference m_ref only moves when some lane's
+    // tile max exceeds it by more than kRescaleSlack, so p = exp2(s - m_ref)
+    // stays <= 2^kRescaleSlack; the result is the same softmax (the common
+    // factor cancels in O / l), and the 64 rescale multiplies are skipped
+    // whenever no lane needs them.
+    if (__ballot(mt > m_ref + kRescaleSlack) != 0) {
+      const float m_new = fmaxf(m_ref, mt);
+      const float alpha = fast_exp2(m_ref - m_new);  // m_ref = -inf -> 0
+      m_ref = m_new;
+      l_run *= alpha;
 #pragma unroll
-    for (int dt = 0; dt < 4; ++dt) oacc[dt] *= alpha;
+      for (int dt = 0; dt < 4; ++dt) oacc[dt] *= alpha;
+    }
+    const float neg_m = (m_ref == -INFINITY) ? 0.f : -m_ref;
 
     uint32_t pk[4][8];
     float ls = 0.f;
@@ -220,8 +233,8 @@ __device__ __forceinline__ void attn_body(bool dense,
     for (int kt = 0; kt < 4; ++kt) {
 #pragma unroll
       for (int r = 0; r < 16; r += 2) {
-        const float p0 = fast_exp2(sacc[kt][r] - m_use);
-        const float p1 = fast_exp2(sacc[kt][r + 1] - m_use);
+        const float p0 = fast_exp2(fmaf(sacc[kt][r], scale_log2, neg_m));
+        const float p1 = fast_exp2(fmaf(sacc[kt][r + 1], scale_log2, neg_m));
         ls += p0 + p1;
         pk[kt][r >> 1] = cvt_pk_bf16(p0, p1);
       }
@@ -283,7 +296,7 @@ __device__ __forceinline__ void attn_body(bool dense,
   }
   if (lse != nullptr && lh == 0)
     lse[(size_t)h * L + qi] =
-        l_tot > 0.f ? (m_run + __builtin_log2f(l_tot)) * 0.69314718055994531f : -INFINITY;
+        l_tot > 0.f ? (m_ref + __builtin_log2f(l_tot)) * 0.69314718055994531f : -INFINITY;
 }
 
 // Dense mode is a runtime flag of the same kernel (not a separate
