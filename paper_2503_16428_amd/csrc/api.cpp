@@ -8,7 +8,7 @@
 #include <cstdio>
 #include <cstring>
 
-#include "../../include/xattn.h"
+#include "xattn.h"
 #include "common.h"
 
 namespace {

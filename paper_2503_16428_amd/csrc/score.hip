@@ -24,10 +24,21 @@ namespace {
 
 constexpr int TM = 256;             // reduced rows (R) and columns (c) per workgroup tile
 constexpr int TSUB = 128;           // column sub-tile owning one (m, l) pair per row
-constexpr int KC = 32;              // reduced-K chunk per pipeline stage
-constexpr int NSTAGE = 4;           // pipeline depth (3 chunks in flight)
+#ifndef XATTN_SCORE_KC
+#define XATTN_SCORE_KC 64
+#endif
+#ifndef XATTN_SCORE_NSTAGE
+#define XATTN_SCORE_NSTAGE 2
+#endif
+constexpr int KC = XATTN_SCORE_KC;          // reduced-K chunk per pipeline stage (32 or 64)
+constexpr int NSTAGE = XATTN_SCORE_NSTAGE;  // pipeline depth: NSTAGE - 1 chunks in flight
 constexpr int kThreads = 512;       // 8 waves: 2 (columns) x 4 (rows), 128 c x 64 R each
-constexpr int kStage = TM * KC;     // bf16 elements of one operand in one stage (32 KB)
+constexpr int kStage = TM * KC;     // bf16 elements of one operand in one stage
+constexpr int kCPR = KC / 8;        // 16-byte chunks per LDS row
+constexpr int kRowsPer256 = 128 / KC;  // LDS rows per 256-byte bank period
+constexpr int kDmaRows = 512 / KC;  // rows one 1 KB direct-to-LDS instruction fills
+constexpr int kDmaPerOp = 32 / kDmaRows;  // instructions per wave per operand per chunk
+static_assert(NSTAGE * 2 * kStage * 2 <= 160 * 1024, "LDS budget");
 
 __host__ __device__ inline int ceil_div(int a, int b) { return (a + b - 1) / b; }
 
@@ -39,9 +50,10 @@ __device__ __forceinline__ void tri_decode(int t, int& rt, int& ct) {
   ct = t - r * (r + 1) / 2;
 }
 
-// LDS rows hold KC = 32 bf16 (4 chunks of 16 B); chunk c of row r sits at
-// position c ^ ((r >> 2) & 3), so 16 consecutive rows read at one logical
-// chunk hit 16 distinct bank groups.
+// LDS rows hold KC bf16 (kCPR chunks of 16 B); chunk c of row r sits at
+// position c ^ ((r / kRowsPer256) mod kCPR), so 16 consecutive rows read at
+// one logical chunk hit 16 distinct bank groups.
+__device__ __forceinline__ int swz_row(int r) { return (r / kRowsPer256) & (kCPR - 1); }
 
 // NRB = reduced rows (and columns) per 128-token block = 128 / S.
 template <int NRB, bool CAUSAL>
@@ -79,13 +91,13 @@ __global__ __launch_bounds__(kThreads, 1) void score_partials(
   const uint16_t* Kg = k + (size_t)gidx * L * kHeadDim;
 
   // ---- direct-to-LDS staging: per stage each wave loads rows 32 wv .. +32 of
-  // both operands, 2 instructions (16 rows x 64 B) each. Rows beyond NR are
-  // clamped to NR - 1 (their results are masked / not stored).
-  uint32_t offA[2], offB[2];
+  // both operands, kDmaPerOp instructions (kDmaRows rows x 2 KC bytes) each.
+  // Rows beyond NR are clamped to NR - 1 (results masked / not stored).
+  uint32_t offA[kDmaPerOp], offB[kDmaPerOp];
 #pragma unroll
-  for (int i = 0; i < 2; ++i) {
-    const int r = 32 * wv + 16 * i + (lane >> 2);
-    const int c = (lane & 3) ^ ((r >> 2) & 3);
+  for (int i = 0; i < kDmaPerOp; ++i) {
+    const int r = 32 * wv + kDmaRows * i + lane / kCPR;
+    const int c = (lane & (kCPR - 1)) ^ swz_row(r);
     const int ra = min(c0 + r, NR - 1), rb = min(R0 + r, NR - 1);
     offA[i] = (uint32_t)(((size_t)ra * KD + c * 8) * 2);
     offB[i] = (uint32_t)(((size_t)rb * S * kHeadDim + c * 8) * 2);
@@ -98,8 +110,8 @@ __global__ __launch_bounds__(kThreads, 1) void score_partials(
     const uint16_t* baseA = Kg + kap0;
     const uint16_t* baseB = Qh + (S - 1 - tsub) * kHeadDim + e0;
 #pragma unroll
-    for (int i = 0; i < 2; ++i) {
-      const uint32_t row_lds = (uint32_t)((32 * wv + 16 * i) * KC * 2);
+    for (int i = 0; i < kDmaPerOp; ++i) {
+      const uint32_t row_lds = (uint32_t)((32 * wv + kDmaRows * i) * KC * 2);
       dma16(baseA, offA[i], st + row_lds);
       dma16(baseB, offB[i], st + kStage * 2 + row_lds);
     }
@@ -114,7 +126,7 @@ __global__ __launch_bounds__(kThreads, 1) void score_partials(
   // Diagonal tiles are computed in full (their masked half is ~2% of the MFMA
   // work of a causal layer); a per-MFMA skip would break the inner loop into
   // branches that serialise every LDS read with its MFMA.
-  const uint32_t xa = (uint32_t)((lr >> 2) & 3);  // swizzle of this lane's rows
+  const uint32_t xa = (uint32_t)swz_row(lr);  // swizzle of this lane's rows (32 t, 64 wr: same)
   auto compute = [&](int ch) {
     const uint16_t* A = lds + (ch % NSTAGE) * 2 * kStage;
     const uint16_t* Bm = A + kStage;
@@ -132,36 +144,46 @@ __global__ __launch_bounds__(kThreads, 1) void score_partials(
         for (int n = 0; n < 2; ++n) acc[t][n] = mfma32(as_bf16x8(ak), as_bf16x8(bq[n]), acc[t][n]);
       }
     }
-    // Issue order per chunk: the 6 reads of k-step 0, then its 8 MFMAs with the
-    // 6 reads of k-step 1 interleaved, then the 8 MFMAs of k-step 1.
+    // Issue order per chunk: the 6 reads of k-step 0, then for each k-step its
+    // 8 MFMAs with the 6 reads of the next k-step interleaved.
     __builtin_amdgcn_sched_group_barrier(0x100, 6, 0);
 #pragma unroll
-    for (int i = 0; i < 6; ++i) {
-      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
-      __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+    for (int k = 0; k + 1 < KC / 16; ++k) {
+#pragma unroll
+      for (int i = 0; i < 6; ++i) {
+        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+        __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+      }
+      __builtin_amdgcn_sched_group_barrier(0x008, 2, 0);
     }
-    __builtin_amdgcn_sched_group_barrier(0x008, 10, 0);
+    __builtin_amdgcn_sched_group_barrier(0x008, 8, 0);
   };
 
-  // Each wave issues 4 loads per chunk; NCH = S*d/32 >= 4 for every stride.
-  // Step ch: wait for chunk ch (chunks ch+1, ch+2 may stay in flight), one
-  // barrier (chunk ch visible; every wave finished chunk ch-1, whose stage
-  // chunk ch+3 now refills), prefetch ch+3, compute ch.
-  issue(0);
-  issue(1);
-  issue(2);
-  for (int ch = 0; ch < NCH - 2; ++ch) {
-    wait_vmcnt<8>();
+  // Each wave issues L = 2 kDmaPerOp loads per chunk (NCH = S d / KC >= NSTAGE).
+  // Step ch: wait for chunk ch (the next NSTAGE - 2 chunks may stay in
+  // flight), one barrier (chunk ch visible; every wave finished chunk ch - 1,
+  // whose stage chunk ch + NSTAGE - 1 now refills), prefetch, compute ch.
+  constexpr int kLoads = 2 * kDmaPerOp;
+  static_assert(NCH >= NSTAGE && NSTAGE >= 2 && NSTAGE <= 4, "pipeline shape");
+#pragma unroll
+  for (int c = 0; c < NSTAGE - 1; ++c) issue(c);
+  for (int ch = 0; ch < NCH - (NSTAGE - 2); ++ch) {
+    wait_vmcnt<kLoads * (NSTAGE - 2)>();
     barrier_nofence();
-    if (ch + 3 < NCH) issue(ch + 3);
+    if (ch + NSTAGE - 1 < NCH) issue(ch + NSTAGE - 1);
     compute(ch);
   }
-  wait_vmcnt<4>();
-  barrier_nofence();
-  compute(NCH - 2);
-  wait_vmcnt<0>();
-  barrier_nofence();
-  compute(NCH - 1);
+  // drain: the last NSTAGE - 2 chunks, each with fewer loads still in flight
+  if constexpr (NSTAGE >= 4) {
+    wait_vmcnt<kLoads>();
+    barrier_nofence();
+    compute(NCH - 2);
+  }
+  if constexpr (NSTAGE >= 3) {
+    wait_vmcnt<0>();
+    barrier_nofence();
+    compute(NCH - 1);
+  }
 
   // ---- epilogue per 32-row slab n: this lane owns reduced row R and 64 of the
   // wave's 128 columns; lane (lr, 1-lh) owns the other 64.
@@ -204,7 +226,9 @@ __global__ __launch_bounds__(kThreads, 1) void score_partials(
     }
     const float l = lloc + __shfl_xor(lloc, 32);
     const bool rvalid = R < NR;
-    float* prow = part + ((size_t)h * NR + (rvalid ? R : 0)) * NB;
+    // part is [head][key block][R]: for one block the 32 lanes of a half-wave
+    // write 32 consecutive rows (one 128-byte segment)
+    float* pcol = part + (size_t)h * NB * NR + (rvalid ? R : 0);
 
     if constexpr (NRB >= 8) {
       // group gi covers columns 8 gi + 4 lh + [0, 4): local block gi / (NRB / 8)
@@ -223,10 +247,10 @@ __global__ __launch_bounds__(kThreads, 1) void score_partials(
 #pragma unroll
           for (int x = 0; x < NBL / 2; ++x) {
             const int jb = lh * (NBL / 2) + x;
-            if (j0 + jb < NB) prow[j0 + jb] = pb[jb];
+            if (j0 + jb < NB) pcol[(size_t)(j0 + jb) * NR] = pb[jb];
           }
         } else {
-          if (lh == 0 && j0 < NB) prow[j0] = pb[0];
+          if (lh == 0 && j0 < NB) pcol[(size_t)j0 * NR] = pb[0];
         }
       }
     } else if constexpr (NRB == 4) {
@@ -235,7 +259,7 @@ __global__ __launch_bounds__(kThreads, 1) void score_partials(
 #pragma unroll
         for (int gi = 0; gi < 16; ++gi) {
           const int j = j0 + 2 * gi + lh;
-          if (j < NB) prow[j] = gsum[gi];
+          if (j < NB) pcol[(size_t)j * NR] = gsum[gi];
         }
       }
     } else {  // NRB == 2: each group holds two blocks
@@ -247,53 +271,96 @@ __global__ __launch_bounds__(kThreads, 1) void score_partials(
           for (int g4 = 0; g4 < 4; ++g4) {
             const int gi = 4 * t + g4;
             const int j = j0 + 4 * gi + 2 * lh;
-            if (j < NB) prow[j] = acc[t][n][4 * g4] + acc[t][n][4 * g4 + 1];
-            if (j + 1 < NB) prow[j + 1] = acc[t][n][4 * g4 + 2] + acc[t][n][4 * g4 + 3];
+            if (j < NB) pcol[(size_t)j * NR] = acc[t][n][4 * g4] + acc[t][n][4 * g4 + 1];
+            if (j + 1 < NB) pcol[(size_t)(j + 1) * NR] = acc[t][n][4 * g4 + 2] + acc[t][n][4 * g4 + 3];
           }
         }
       }
     }
     if (rvalid && lh == 0 && tsub_idx < NT)
-      stats[((size_t)h * NR + R) * NT + tsub_idx] = make_float2(m, l);
+      stats[((size_t)h * NT + tsub_idx) * NR + R] = make_float2(m, l);
   }
 }
 
-// One workgroup per (query head, query block) row.
+__device__ __forceinline__ float wave_max(float x) {
+#pragma unroll
+  for (int off = 32; off >= 1; off >>= 1) x = fmaxf(x, __shfl_xor(x, off));
+  return x;
+}
+__device__ __forceinline__ float wave_sum(float x) {
+#pragma unroll
+  for (int off = 32; off >= 1; off >>= 1) x += __shfl_xor(x, off);
+  return x;
+}
+
+constexpr int kFacMax = 1024;  // LDS factors f[r][t] (4 KB) when nrb * tiles fits
+
+// One workgroup (4 waves) per (query head, query block) row. For each of the
+// row's nrb reduced rows R: m_R = max_t m[t][R], l_R = sum_t l[t][R] 2^(m - m_R)
+// (one wave per row, lanes over tiles, fixed reduction order); then
+// f[r][t] = 2^(m[t][R] - m_R) / l_R and
+//   score[h][b][j] = (1/nrb) sum_r part[j][R] f[r][t(j)].
 template <bool CAUSAL>
 __global__ __launch_bounds__(256) void score_finalize(const float* __restrict__ part,
                                                       const float2* __restrict__ stats, int NR,
                                                       int NB, int NT, int nrb,
                                                       float* __restrict__ scores) {
   const int h = blockIdx.x / NB, b = blockIdx.x % NB;
+  const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
   __shared__ float mR[kBlock], ilR[kBlock];
-  const int tid = threadIdx.x;
-  if (tid < nrb) {
-    const int R = b * nrb + tid;
-    const int tmax = CAUSAL ? R / TSUB : NT - 1;
-    const float2* st = stats + ((size_t)h * NR + R) * NT;
+  __shared__ float fac[kFacMax];
+  const int ncand = CAUSAL ? b + 1 : NB;
+  const int tj = ((ncand - 1) * nrb) / TSUB + 1;  // tiles holding candidate blocks
+  const float2* st = stats + (size_t)h * NT * NR;
+  for (int r = wv; r < nrb; r += 4) {
+    const int R = b * nrb + r;
+    const int tn = CAUSAL ? R / TSUB + 1 : NT;
     float m = -INFINITY;
-    for (int t = 0; t <= tmax; ++t) m = fmaxf(m, st[t].x);
+    for (int t = lane; t < tn; t += 64) m = fmaxf(m, st[(size_t)t * NR + R].x);
+    m = wave_max(m);
     float l = 0.f;
-    for (int t = 0; t <= tmax; ++t) l += st[t].y * fast_exp2(st[t].x - m);
-    mR[tid] = m;
-    ilR[tid] = 1.f / l;
+    for (int t = lane; t < tn; t += 64) {
+      const float2 v = st[(size_t)t * NR + R];
+      l += v.y * fast_exp2(v.x - m);
+    }
+    l = wave_sum(l);
+    if (lane == 0) {
+      mR[r] = m;
+      ilR[r] = 1.f / l;
+    }
   }
   __syncthreads();
-  const int ncand = CAUSAL ? b + 1 : NB;
+  const bool lds_fac = nrb * tj <= kFacMax;
+  if (lds_fac) {
+    for (int i = tid; i < nrb * tj; i += 256) {
+      const int r = i / tj, t = i % tj;
+      fac[i] = fast_exp2(st[(size_t)t * NR + b * nrb + r].x - mR[r]) * ilR[r];
+    }
+    __syncthreads();
+  }
+  // Threads take (block j, row r) pairs with r fastest, G = min(nrb, 64) lanes
+  // per block: a wave reads 64 / G runs of G consecutive rows (G * 4 bytes
+  // each), then the G lanes of a block reduce over r with shuffles.
+  const int G = nrb < 64 ? nrb : 64;
+  const int jpp = 256 / G;  // blocks per pass
+  const int g = tid % G;
   const float inv_nrb = 1.f / (float)nrb;
   float* out = scores + ((size_t)h * NB + b) * NB;
-  for (int j = tid; j < NB; j += 256) {
+  const float* pb = part + (size_t)h * NB * NR + (size_t)b * nrb;
+  for (int j0 = 0; j0 < NB; j0 += jpp) {
+    const int j = j0 + tid / G;
     float acc = 0.f;
     if (j < ncand) {
       const int t = (j * nrb) / TSUB;
-      for (int r = 0; r < nrb; ++r) {
-        const size_t R = (size_t)h * NR + b * nrb + r;
-        const float f = fast_exp2(stats[R * NT + t].x - mR[r]) * ilR[r];
-        acc += part[R * NB + j] * f;
+      const float* pj = pb + (size_t)j * NR;
+      for (int r = g; r < nrb; r += G) {
+        const float f = lds_fac ? fac[r * tj + t]
+                                : fast_exp2(st[(size_t)t * NR + b * nrb + r].x - mR[r]) * ilR[r];
+        acc += pj[r] * f;
       }
-      acc *= inv_nrb;
     }
-    out[j] = acc;
+    for (int off = G / 2; off >= 1; off >>= 1) acc += __shfl_xor(acc, off);
+    if (g == 0 && j < NB) out[j] = acc * inv_nrb;
   }
 }
 
