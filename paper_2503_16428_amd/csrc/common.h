@@ -57,11 +57,15 @@ __device__ __forceinline__ void wait_vmcnt() {
   asm volatile("s_waitcnt vmcnt(%0)" ::"n"(N) : "memory");
 }
 
-// Workgroup barrier without a memory fence: LDS tiles are ordered explicitly
-// (each wave waits for its own direct-to-LDS loads before the barrier, and
-// every LDS read has been consumed before the barrier that frees a buffer);
-// __syncthreads would also wait for prefetches meant to stay in flight.
-__device__ __forceinline__ void barrier_nofence() { asm volatile("s_barrier" ::: "memory"); }
+// Workgroup barrier that does not wait for vector-memory loads (prefetches
+// into LDS stay in flight; __syncthreads would drain them). Each wave first
+// waits for its own outstanding LDS reads (lgkmcnt(0)): the compiler may sink
+// the instruction consuming a ds_read below the barrier, and without the wait
+// another wave could refill the buffer before that read returns. Waiting for
+// a wave's own direct-to-LDS loads (vmcnt) is left to the caller.
+__device__ __forceinline__ void barrier_nofence() {
+  asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
+}
 
 #define XATTN_LDS_ADDR(p) ((uint32_t)(uintptr_t)((__attribute__((address_space(3))) void*)(p)))
 
