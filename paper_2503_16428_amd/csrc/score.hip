@@ -226,9 +226,11 @@ __global__ __launch_bounds__(kThreads, 1) void score_partials(
     }
     const float l = lloc + __shfl_xor(lloc, 32);
     const bool rvalid = R < NR;
-    // part is [head][key block][R]: for one block the 32 lanes of a half-wave
-    // write 32 consecutive rows (one 128-byte segment)
-    float* pcol = part + (size_t)h * NB * NR + (rvalid ? R : 0);
+    // part is [head][query block][key block][row in block]: what the
+    // finalize workgroup of one query block reads is one contiguous slab;
+    // a half-wave writes 32 / NRB runs of NRB consecutive floats per block.
+    const int Rv = rvalid ? R : 0;
+    float* pcol = part + ((size_t)(h * NB + Rv / NRB) * NB) * NRB + (Rv % NRB);
 
     if constexpr (NRB >= 8) {
       // group gi covers columns 8 gi + 4 lh + [0, 4): local block gi / (NRB / 8)
@@ -247,10 +249,10 @@ __global__ __launch_bounds__(kThreads, 1) void score_partials(
 #pragma unroll
           for (int x = 0; x < NBL / 2; ++x) {
             const int jb = lh * (NBL / 2) + x;
-            if (j0 + jb < NB) pcol[(size_t)(j0 + jb) * NR] = pb[jb];
+            if (j0 + jb < NB) pcol[(size_t)(j0 + jb) * NRB] = pb[jb];
           }
         } else {
-          if (lh == 0 && j0 < NB) pcol[(size_t)j0 * NR] = pb[0];
+          if (lh == 0 && j0 < NB) pcol[(size_t)j0 * NRB] = pb[0];
         }
       }
     } else if constexpr (NRB == 4) {
@@ -259,7 +261,7 @@ __global__ __launch_bounds__(kThreads, 1) void score_partials(
 #pragma unroll
         for (int gi = 0; gi < 16; ++gi) {
           const int j = j0 + 2 * gi + lh;
-          if (j < NB) pcol[(size_t)j * NR] = gsum[gi];
+          if (j < NB) pcol[(size_t)j * NRB] = gsum[gi];
         }
       }
     } else {  // NRB == 2: each group holds two blocks
@@ -271,8 +273,8 @@ __global__ __launch_bounds__(kThreads, 1) void score_partials(
           for (int g4 = 0; g4 < 4; ++g4) {
             const int gi = 4 * t + g4;
             const int j = j0 + 4 * gi + 2 * lh;
-            if (j < NB) pcol[(size_t)j * NR] = acc[t][n][4 * g4] + acc[t][n][4 * g4 + 1];
-            if (j + 1 < NB) pcol[(size_t)(j + 1) * NR] = acc[t][n][4 * g4 + 2] + acc[t][n][4 * g4 + 3];
+            if (j < NB) pcol[(size_t)j * NRB] = acc[t][n][4 * g4] + acc[t][n][4 * g4 + 1];
+            if (j + 1 < NB) pcol[(size_t)(j + 1) * NRB] = acc[t][n][4 * g4 + 2] + acc[t][n][4 * g4 + 3];
           }
         }
       }
@@ -339,20 +341,20 @@ __global__ __launch_bounds__(256) void score_finalize(const float* __restrict__ 
     __syncthreads();
   }
   // Threads take (block j, row r) pairs with r fastest, G = min(nrb, 64) lanes
-  // per block: a wave reads 64 / G runs of G consecutive rows (G * 4 bytes
-  // each), then the G lanes of a block reduce over r with shuffles.
+  // per block: a wave reads 64 consecutive floats of the slab, then the G
+  // lanes of a block reduce over r with shuffles.
   const int G = nrb < 64 ? nrb : 64;
   const int jpp = 256 / G;  // blocks per pass
   const int g = tid % G;
   const float inv_nrb = 1.f / (float)nrb;
   float* out = scores + ((size_t)h * NB + b) * NB;
-  const float* pb = part + (size_t)h * NB * NR + (size_t)b * nrb;
+  const float* pb = part + ((size_t)(h * NB + b) * NB) * nrb;  // this row's slab [j][r]
   for (int j0 = 0; j0 < NB; j0 += jpp) {
     const int j = j0 + tid / G;
     float acc = 0.f;
     if (j < ncand) {
       const int t = (j * nrb) / TSUB;
-      const float* pj = pb + (size_t)j * NR;
+      const float* pj = pb + (size_t)j * nrb;
       for (int r = g; r < nrb; r += G) {
         const float f = lds_fac ? fac[r * tj + t]
                                 : fast_exp2(st[(size_t)t * NR + b * nrb + r].x - mR[r]) * ilR[r];
