@@ -295,13 +295,20 @@ __device__ __forceinline__ float wave_sum(float x) {
   return x;
 }
 
-constexpr int kFacMax = 1024;  // LDS factors f[r][t] (4 KB) when nrb * tiles fits
+constexpr int kStatMax = 2048;  // (row, tile) stats staged in LDS (16 KB) when they fit
+constexpr int kFinUnroll = 4;   // independent 16-byte partial-sum loads per thread
 
-// One workgroup (4 waves) per (query head, query block) row. For each of the
-// row's nrb reduced rows R: m_R = max_t m[t][R], l_R = sum_t l[t][R] 2^(m - m_R)
-// (one wave per row, lanes over tiles, fixed reduction order); then
-// f[r][t] = 2^(m[t][R] - m_R) / l_R and
+// One workgroup (4 waves) per (query head, query block) row, nrb = B/S
+// reduced rows R = b nrb + r and tn column sub-tiles per row:
+//   m_R = max_t m[t][R],  l_R = sum_t l[t][R] 2^(m[t][R] - m_R),
+//   f[r][t] = 2^(m[t][R] - m_R) / l_R,
 //   score[h][b][j] = (1/nrb) sum_r part[j][R] f[r][t(j)].
+// The (r, t) stats are read r-fastest (the nrb rows of one tile are adjacent
+// in memory) into LDS; one wave per row reduces them in a fixed order. The
+// row's partial-sum slab [j][r] is streamed as float4 (or float2 when nrb =
+// 2), kFinUnroll loads in flight per thread; the nrb / 4 lanes of one block
+// then reduce with shuffles in a fixed order. Rows whose stats exceed the LDS
+// stage use the same arithmetic with the stats read from global memory.
 template <bool CAUSAL>
 __global__ __launch_bounds__(256) void score_finalize(const float* __restrict__ part,
                                                       const float2* __restrict__ stats, int NR,
@@ -310,19 +317,29 @@ __global__ __launch_bounds__(256) void score_finalize(const float* __restrict__ 
   const int h = blockIdx.x / NB, b = blockIdx.x % NB;
   const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
   __shared__ float mR[kBlock], ilR[kBlock];
-  __shared__ float fac[kFacMax];
+  __shared__ float sm[kStatMax], sl[kStatMax];  // sm[t * nrb + r]: m, then the factor f
   const int ncand = CAUSAL ? b + 1 : NB;
-  const int tj = ((ncand - 1) * nrb) / TSUB + 1;  // tiles holding candidate blocks
-  const float2* st = stats + (size_t)h * NT * NR;
+  const int tn = CAUSAL ? (b * nrb) / TSUB + 1 : NT;  // sub-tiles of this row's stats
+  const float2* st = stats + (size_t)h * NT * NR + (size_t)b * nrb;  // + t * NR + r
+  const bool staged = nrb * tn <= kStatMax;
+  if (staged) {
+    for (int i = tid; i < nrb * tn; i += 256) {
+      const int t = i / nrb, r = i - t * nrb;
+      const float2 v = st[(size_t)t * NR + r];
+      sm[i] = v.x;
+      sl[i] = v.y;
+    }
+    __syncthreads();
+  }
   for (int r = wv; r < nrb; r += 4) {
-    const int R = b * nrb + r;
-    const int tn = CAUSAL ? R / TSUB + 1 : NT;
     float m = -INFINITY;
-    for (int t = lane; t < tn; t += 64) m = fmaxf(m, st[(size_t)t * NR + R].x);
+    for (int t = lane; t < tn; t += 64)
+      m = fmaxf(m, staged ? sm[t * nrb + r] : st[(size_t)t * NR + r].x);
     m = wave_max(m);
     float l = 0.f;
     for (int t = lane; t < tn; t += 64) {
-      const float2 v = st[(size_t)t * NR + R];
+      const float2 v = staged ? make_float2(sm[t * nrb + r], sl[t * nrb + r])
+                              : st[(size_t)t * NR + r];
       l += v.y * fast_exp2(v.x - m);
     }
     l = wave_sum(l);
@@ -332,38 +349,65 @@ __global__ __launch_bounds__(256) void score_finalize(const float* __restrict__ 
     }
   }
   __syncthreads();
-  const bool lds_fac = nrb * tj <= kFacMax;
-  if (lds_fac) {
-    for (int i = tid; i < nrb * tj; i += 256) {
-      const int r = i / tj, t = i % tj;
-      fac[i] = fast_exp2(st[(size_t)t * NR + b * nrb + r].x - mR[r]) * ilR[r];
+  if (staged) {
+    for (int i = tid; i < nrb * tn; i += 256) {
+      const int r = i % nrb;
+      sm[i] = fast_exp2(sm[i] - mR[r]) * ilR[r];
     }
     __syncthreads();
   }
-  // Threads take (block j, row r) pairs with r fastest, G = min(nrb, 64) lanes
-  // per block: a wave reads 64 consecutive floats of the slab, then the G
-  // lanes of a block reduce over r with shuffles.
-  const int G = nrb < 64 ? nrb : 64;
-  const int jpp = 256 / G;  // blocks per pass
-  const int g = tid % G;
+  auto factor = [&](int r, int t) -> float {
+    return staged ? sm[t * nrb + r] : fast_exp2(st[(size_t)t * NR + r].x - mR[r]) * ilR[r];
+  };
+
   const float inv_nrb = 1.f / (float)nrb;
   float* out = scores + ((size_t)h * NB + b) * NB;
   const float* pb = part + ((size_t)(h * NB + b) * NB) * nrb;  // this row's slab [j][r]
-  for (int j0 = 0; j0 < NB; j0 += jpp) {
-    const int j = j0 + tid / G;
-    float acc = 0.f;
-    if (j < ncand) {
-      const int t = (j * nrb) / TSUB;
-      const float* pj = pb + (size_t)j * nrb;
-      for (int r = g; r < nrb; r += G) {
-        const float f = lds_fac ? fac[r * tj + t]
-                                : fast_exp2(st[(size_t)t * NR + b * nrb + r].x - mR[r]) * ilR[r];
-        acc += pj[r] * f;
+  if (nrb >= 4) {
+    // chunk q = 4 consecutive floats = rows 4 (q % (nrb/4)) .. +3 of block q / (nrb/4)
+    const int cpb = nrb / 4;  // chunks (lanes) per block, a power of two <= 32
+    const int nq = ncand * cpb;
+    const float4* p4 = (const float4*)pb;
+    for (int q0 = 0; q0 < nq; q0 += 256 * kFinUnroll) {
+      float4 v[kFinUnroll];
+#pragma unroll
+      for (int u = 0; u < kFinUnroll; ++u) {
+        const int q = q0 + 256 * u + tid;
+        v[u] = q < nq ? p4[q] : make_float4(0.f, 0.f, 0.f, 0.f);
+      }
+#pragma unroll
+      for (int u = 0; u < kFinUnroll; ++u) {
+        const int q = q0 + 256 * u + tid;
+        const int j = q / cpb, r0 = 4 * (q % cpb);
+        const int t = (j * nrb) / TSUB;
+        float acc = 0.f;
+        if (q < nq)
+          acc = v[u].x * factor(r0, t) + v[u].y * factor(r0 + 1, t) +
+                v[u].z * factor(r0 + 2, t) + v[u].w * factor(r0 + 3, t);
+        for (int off = cpb / 2; off >= 1; off >>= 1) acc += __shfl_xor(acc, off);
+        if (q < nq && (q % cpb) == 0) out[j] = acc * inv_nrb;
       }
     }
-    for (int off = G / 2; off >= 1; off >>= 1) acc += __shfl_xor(acc, off);
-    if (g == 0 && j < NB) out[j] = acc * inv_nrb;
+  } else {  // nrb == 2: one float2 per block
+    const float2* p2 = (const float2*)pb;
+    for (int j0 = 0; j0 < ncand; j0 += 256 * kFinUnroll) {
+      float2 v[kFinUnroll];
+#pragma unroll
+      for (int u = 0; u < kFinUnroll; ++u) {
+        const int j = j0 + 256 * u + tid;
+        v[u] = j < ncand ? p2[j] : make_float2(0.f, 0.f);
+      }
+#pragma unroll
+      for (int u = 0; u < kFinUnroll; ++u) {
+        const int j = j0 + 256 * u + tid;
+        if (j < ncand) {
+          const int t = (j * nrb) / TSUB;
+          out[j] = (v[u].x * factor(0, t) + v[u].y * factor(1, t)) * inv_nrb;
+        }
+      }
+    }
   }
+  for (int j = ncand + tid; j < NB; j += 256) out[j] = 0.f;  // not candidates
 }
 
 template <int NRB, bool CAUSAL>
