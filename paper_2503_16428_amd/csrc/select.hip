@@ -18,36 +18,31 @@ using namespace xattn;
 
 namespace {
 
-__device__ __forceinline__ uint64_t wave_sum_u64(uint64_t x) {
-#pragma unroll
-  for (int off = 32; off >= 1; off >>= 1) {
-    const uint32_t lo = __shfl_xor((uint32_t)x, off);
-    const uint32_t hi = __shfl_xor((uint32_t)(x >> 32), off);
-    x += ((uint64_t)hi << 32) | lo;
-  }
-  return x;
+// Sum over the wave, returned uniform (in a scalar register): prefix sums
+// inside each row of 16 lanes by DPP row shifts, then the four row totals.
+__device__ __forceinline__ uint32_t wave_sum_u32(uint32_t x) {
+  x += __builtin_amdgcn_update_dpp(0u, x, 0x111, 0xf, 0xf, false);  // row_shr:1
+  x += __builtin_amdgcn_update_dpp(0u, x, 0x112, 0xf, 0xf, false);  // row_shr:2
+  x += __builtin_amdgcn_update_dpp(0u, x, 0x114, 0xf, 0xf, false);  // row_shr:4
+  x += __builtin_amdgcn_update_dpp(0u, x, 0x118, 0xf, 0xf, false);  // row_shr:8
+  return __builtin_amdgcn_readlane(x, 15) + __builtin_amdgcn_readlane(x, 31) +
+         __builtin_amdgcn_readlane(x, 47) + __builtin_amdgcn_readlane(x, 63);
 }
 
-// NPL = candidate slots per lane (64 * NPL >= NB); lane l holds j = l + 64 i.
-template <int NPL, bool CAUSAL>
-__global__ __launch_bounds__(256) void select_kernel(const float* __restrict__ scores,
-                                                     int n_rows, int NB, float tau,
-                                                     int32_t* __restrict__ idx,
-                                                     int32_t* __restrict__ cnt) {
-  const int lane = threadIdx.x & 63;
-  const int row = blockIdx.x * 4 + (threadIdx.x >> 6);
-  if (row >= n_rows) return;  // uniform per wave
-  const int b = row % NB;
-  const int m = CAUSAL ? b + 1 : NB;
-  const float* s = scores + (size_t)row * NB;
-  int32_t* out = idx + (size_t)row * NB;
+// Exact wave sum of per-lane values below 2^42: the high and low 21-bit parts
+// are summed separately (each total stays below 2^27).
+__device__ __forceinline__ uint64_t wave_sum_u64(uint64_t x) {
+  const uint32_t hi = wave_sum_u32((uint32_t)(x >> 21));
+  const uint32_t lo = wave_sum_u32((uint32_t)x & ((1u << 21) - 1u));
+  return ((uint64_t)hi << 21) + lo;
+}
 
-  if (tau >= 1.f) {
-    for (int j = lane; j < m; j += 64) out[j] = j;
-    if (lane == 0) cnt[row] = m;
-    return;
-  }
-
+// One row with at most 64 NPL candidates; lane l holds j = l + 64 i. Every
+// per-lane partial sum below is at most NPL * 2^32 <= 2^37.
+template <int NPL>
+__device__ __forceinline__ void select_row(const float* __restrict__ s, int m, float tau,
+                                           int lane, int32_t* __restrict__ out,
+                                           int32_t* __restrict__ cnt_out) {
   uint64_t u[NPL];
   uint64_t tl = 0;
 #pragma unroll
@@ -62,7 +57,7 @@ __global__ __launch_bounds__(256) void select_kernel(const float* __restrict__ s
   if (T == 0) {  // every candidate has zero mass: the first in (u desc, j asc) order is j = 0
     if (lane == 0) {
       out[0] = 0;
-      cnt[row] = 1;
+      *cnt_out = 1;
     }
     return;
   }
@@ -101,7 +96,37 @@ __global__ __launch_bounds__(256) void select_kernel(const float* __restrict__ s
     written += __popcll(smask);
     ties_seen += __popcll(tmask);
   }
-  if (lane == 0) cnt[row] = (int32_t)written;
+  if (lane == 0) *cnt_out = (int32_t)written;
+}
+
+// One wave64 per (head, query block) row. NPL = slots per lane for the
+// longest row (64 NPL >= NB); a causal row with m = b + 1 candidates runs the
+// smallest power-of-two slot count that holds them.
+template <int NPL, bool CAUSAL>
+__global__ __launch_bounds__(256) void select_kernel(const float* __restrict__ scores,
+                                                     int n_rows, int NB, float tau,
+                                                     int32_t* __restrict__ idx,
+                                                     int32_t* __restrict__ cnt) {
+  const int lane = threadIdx.x & 63;
+  const int row = blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (row >= n_rows) return;  // uniform per wave
+  const int b = row % NB;
+  const int m = CAUSAL ? b + 1 : NB;
+  const float* s = scores + (size_t)row * NB;
+  int32_t* out = idx + (size_t)row * NB;
+
+  if (tau >= 1.f) {
+    for (int j = lane; j < m; j += 64) out[j] = j;
+    if (lane == 0) cnt[row] = m;
+    return;
+  }
+  const int nact = (m + 63) >> 6;
+  if (NPL <= 1 || nact <= 1) select_row<1>(s, m, tau, lane, out, cnt + row);
+  else if (NPL <= 2 || nact <= 2) select_row<(NPL < 2 ? NPL : 2)>(s, m, tau, lane, out, cnt + row);
+  else if (NPL <= 4 || nact <= 4) select_row<(NPL < 4 ? NPL : 4)>(s, m, tau, lane, out, cnt + row);
+  else if (NPL <= 8 || nact <= 8) select_row<(NPL < 8 ? NPL : 8)>(s, m, tau, lane, out, cnt + row);
+  else if (NPL <= 16 || nact <= 16) select_row<(NPL < 16 ? NPL : 16)>(s, m, tau, lane, out, cnt + row);
+  else select_row<NPL>(s, m, tau, lane, out, cnt + row);
 }
 
 template <int NPL>
