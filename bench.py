@@ -204,6 +204,7 @@ def main():
     dom = max(kernels, key=lambda n: kernels[n]["ms"])
     ach = kernels[dom]["flops"] / (kernels[dom]["ms"] * 1e-3) / 1e12
     traffic = read_traffic(a.traffic_file, w, dom)
+    attn_traffic = read_traffic(a.traffic_file, w, "attn")
     roofline = {"bound": "mfma", "kernel": dom, "achieved": round(ach, 2),
                 "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s", "frac": round(ach / PEAK_BF16_TFLOPS, 4),
                 "traffic": traffic,
@@ -242,6 +243,9 @@ def main():
         "attn_mfma_frac_computed_blocks": round(attn_flops / (t_attn * 1e-3) / 1e12 /
                                                 PEAK_BF16_TFLOPS, 4),
         "score_mfma_frac": round(score_flops / (t_score * 1e-3) / 1e12 / PEAK_BF16_TFLOPS, 4),
+        # K/V (+ Q, O) stream of the attention kernel: profiled HBM bytes per launch / time
+        "attn_hbm_GBps": (None if attn_traffic is None else
+                          round(attn_traffic / (t_attn * 1e-3) / 1e9, 1)),
         "roofline": roofline,
         "cpu_baseline": cpu,
     }

@@ -78,19 +78,6 @@ __device__ __forceinline__ int xcd_remap(int bid, int n) {
   return x * per + (x < rem ? x : rem) + k;
 }
 
-// Bijection blockIdx -> logical work index that hands each XCD runs of C
-// consecutive logical items while the 8 XCDs together still sweep the logical
-// order front to back: the k-th workgroup that XCD x receives (blockIdx = 8k
-// + x) takes item ((k / C) * 8 + x) * C + k % C. Items that share inputs and
-// sit within C of each other then share one L2; the tail that does not fill
-// 8 C items keeps the identity mapping.
-__device__ __forceinline__ int xcd_chunk_remap(int bid, int n, int C) {
-  const int n_full = n / (kNumXcd * C) * (kNumXcd * C);
-  if (bid >= n_full) return bid;
-  const int x = bid % kNumXcd, k = bid / kNumXcd;
-  return ((k / C) * kNumXcd + x) * C + k % C;
-}
-
 }  // namespace xattn
 
 // Kernel launchers (one per .hip file), called by the C ABI layer after the
