@@ -50,6 +50,8 @@ def lib():
         L.oracle_num_threads.restype = i
         L.oracle_score_rows.argtypes = [P, P, P, i, i, i, P, P, P]
         L.oracle_select_rows.argtypes = [P, i, i, i, P, ctypes.c_float, P, P]
+        L.oracle_select_topk_rows.argtypes = [P, i, i, i, P, P, P, P]
+        L.oracle_select_ratio_rows.argtypes = [P, i, i, i, P, P, P, P]
         L.oracle_sparse_attn_rows.argtypes = [P, P, P, P, i, i, P, P, P, i, P, P, P]
         L.oracle_dense_attn_rows.argtypes = [P, P, P, P, i, i, P, P, P, P]
         L.oracle_block_mass_rows.argtypes = [P, P, P, i, i, i, P, P, P, P]
@@ -111,6 +113,46 @@ def select_rows(scores, row_b, tau, causal=True):
     cnt = np.zeros(n, dtype=np.int32)
     lib().oracle_select_rows(_ptr(s), NB, 1 if causal else 0, n, _ptr(rb),
                              ctypes.c_float(tau), _ptr(idx), _ptr(cnt))
+    return idx, cnt
+
+
+def select_heads_rows(scores, row_h, row_b, tau_h, hq, causal=True):
+    """find_blocks with a threshold per query head: row i uses tau_h[row_h[i] % hq]."""
+    s = np.ascontiguousarray(scores, dtype=np.float64)
+    row_h = np.asarray(row_h)
+    n, NB = s.shape
+    idx = np.full((n, NB), -1, dtype=np.int32)
+    cnt = np.zeros(n, dtype=np.int32)
+    for hh in np.unique(row_h % hq):
+        sel = np.nonzero(row_h % hq == hh)[0]
+        i2, c2 = select_rows(s[sel], np.asarray(row_b)[sel], float(np.float32(tau_h[hh])), causal)
+        idx[sel], cnt[sel] = i2, c2
+    return idx, cnt
+
+
+def select_topk_rows(scores, row_b, k_row, causal=True):
+    """The k_row[i] first candidates of row i in (mass desc, j asc) order."""
+    s = np.ascontiguousarray(scores, dtype=np.float64)
+    rb = np.ascontiguousarray(row_b, dtype=np.int32)
+    n, NB = s.shape
+    kr = np.ascontiguousarray(np.broadcast_to(np.asarray(k_row, dtype=np.int32), (n,)))
+    idx = np.full((n, NB), -1, dtype=np.int32)
+    cnt = np.zeros(n, dtype=np.int32)
+    lib().oracle_select_topk_rows(_ptr(s), NB, 1 if causal else 0, n, _ptr(rb), _ptr(kr),
+                                  _ptr(idx), _ptr(cnt))
+    return idx, cnt
+
+
+def select_ratio_rows(scores, row_b, ratio_row, causal=True):
+    """Top-Ratio: round(ratio * candidates) blocks per row (at least one)."""
+    s = np.ascontiguousarray(scores, dtype=np.float64)
+    rb = np.ascontiguousarray(row_b, dtype=np.int32)
+    n, NB = s.shape
+    rr = np.ascontiguousarray(np.broadcast_to(np.asarray(ratio_row, dtype=np.float32), (n,)))
+    idx = np.full((n, NB), -1, dtype=np.int32)
+    cnt = np.zeros(n, dtype=np.int32)
+    lib().oracle_select_ratio_rows(_ptr(s), NB, 1 if causal else 0, n, _ptr(rb), _ptr(rr),
+                                   _ptr(idx), _ptr(cnt))
     return idx, cnt
 
 

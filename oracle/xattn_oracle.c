@@ -176,6 +176,57 @@ void oracle_select_rows(const double *scores, int NB, int causal, int nrows,
     }
 }
 
+/*
+ * Fixed-size selection (Sec. 4.5, Top-K vs. Top-Ratio ablation, Table 6): per
+ * row keep the k_row[i] candidates that come first in the same (u desc,
+ * j asc) order as find_blocks, u = floor(clamp(score, 0, 1) * 2^32); k is
+ * clamped to [1, m] (m candidates), the output sorted ascending.
+ */
+void oracle_select_topk_rows(const double *scores, int NB, int causal, int nrows,
+                             const int32_t *row_b, const int32_t *k_row, int32_t *idx,
+                             int32_t *cnt)
+{
+#pragma omp parallel for schedule(dynamic, 16)
+    for (int i = 0; i < nrows; ++i) {
+        const int m = causal ? row_b[i] + 1 : NB;
+        const double *s = scores + (size_t)i * NB;
+        int32_t *out = idx + (size_t)i * NB;
+        for (int j = 0; j < NB; ++j) out[j] = -1;
+        int k = k_row[i] < 1 ? 1 : (k_row[i] > m ? m : k_row[i]);
+        cand *c = (cand *)malloc(sizeof(cand) * m);
+        for (int j = 0; j < m; ++j) {
+            double v = s[j] > 0.0 ? (s[j] < 1.0 ? s[j] : 1.0) : 0.0;
+            c[j].u = (uint64_t)floor(v * 4294967296.0);
+            c[j].j = j;
+        }
+        qsort(c, (size_t)m, sizeof(cand), cand_cmp);
+        for (int t = 0; t < k; ++t) out[t] = c[t].j;
+        qsort(out, (size_t)k, sizeof(int32_t), int_cmp);
+        cnt[i] = k;
+        free(c);
+    }
+}
+
+/*
+ * Top-Ratio: the block count of a row is the fraction ratio of its m
+ * candidates, rounded to the nearest whole block (halves up) and clamped to
+ * [1, m]; ratio is the caller's fp32 value, the product taken in fp64. Then
+ * as Top-K.
+ */
+void oracle_select_ratio_rows(const double *scores, int NB, int causal, int nrows,
+                              const int32_t *row_b, const float *ratio_row, int32_t *idx,
+                              int32_t *cnt)
+{
+    int32_t *k = (int32_t *)malloc(sizeof(int32_t) * (nrows > 0 ? nrows : 1));
+    for (int i = 0; i < nrows; ++i) {
+        const int m = causal ? row_b[i] + 1 : NB;
+        const double want = floor((double)ratio_row[i] * (double)m + 0.5);
+        k[i] = want < 1.0 ? 1 : (want > (double)m ? m : (int32_t)want);
+    }
+    oracle_select_topk_rows(scores, NB, causal, nrows, row_b, k, idx, cnt);
+    free(k);
+}
+
 /* softmax(q.k/sqrt(d)) v over an explicit key list, one query. */
 static void attend_one(const uint16_t *qi, const uint16_t *K, const uint16_t *V, int D,
                        const int32_t *keys, int nk, double *sbuf, double *o, double *lse)

@@ -37,6 +37,16 @@ MUTANTS = [
      "const int nk = d->causal ? (qi > 0 ? qi : 1) : L;\n            for (int kk = 0; kk < nk; ++kk) keys[kk] = kk;"),
     ("attn_value_row_wrong", "const uint16_t *vr = V + (size_t)keys[t] * D;",
      "const uint16_t *vr = V + (size_t)(nk - 1 - t) * D;"),
+    ("topk_takes_the_tail", "for (int t = 0; t < k; ++t) out[t] = c[t].j;",
+     "for (int t = 0; t < k; ++t) out[t] = c[m - 1 - t].j;"),
+    ("topk_output_unsorted", "qsort(out, (size_t)k, sizeof(int32_t), int_cmp);\n        cnt[i] = k;",
+     "cnt[i] = k;"),
+    ("topk_off_by_one", "for (int t = 0; t < k; ++t) out[t] = c[t].j;",
+     "for (int t = 0; t < k; ++t) out[t] = c[t + (t + 1 < m)].j;"),
+    ("ratio_rounds_up", "floor((double)ratio_row[i] * (double)m + 0.5)",
+     "ceil((double)ratio_row[i] * (double)m)"),
+    ("ratio_rounds_down", "floor((double)ratio_row[i] * (double)m + 0.5)",
+     "floor((double)ratio_row[i] * (double)m)"),
 ]
 
 PINS = [
@@ -54,7 +64,12 @@ PINS = [
     lambda: P.test_dense_matches_torch_sdpa(True),
     lambda: P.test_sparse_equals_block_masked_attention(True),
     P.test_zero_query_attention_is_running_mean_of_values,
-]
+    lambda: P.test_topk_is_the_upper_set_of_the_selection_order(False),
+    lambda: P.test_topk_is_the_upper_set_of_the_selection_order(True),
+    P.test_topk_sets_nest_and_match_threshold_selection_at_its_count,
+    P.test_topk_brute_force_mass_is_maximal,
+] + [lambda a=a: P.test_ratio_block_count_rounds_to_nearest(*a) for a in [
+    (0.5, 3, 2), (0.27, 100, 27), (0.7, 10, 7), (0.01, 3, 1), (2.0, 4, 4)]]
 
 
 def _build_mutant(tmp_path, name, old, new):
@@ -74,7 +89,8 @@ def test_pins_catch_mutant(tmp_path, name, old, new):
     real = oracle.lib()
     L = ctypes.CDLL(lib_path)
     for f in ("oracle_score_rows", "oracle_select_rows", "oracle_sparse_attn_rows",
-              "oracle_dense_attn_rows", "oracle_block_mass_rows"):
+              "oracle_dense_attn_rows", "oracle_block_mass_rows", "oracle_select_topk_rows",
+              "oracle_select_ratio_rows"):
         getattr(L, f).argtypes = getattr(real, f).argtypes
     L.oracle_num_threads.restype = ctypes.c_int
     caught = []

@@ -261,6 +261,88 @@ def test_select_monotone_in_tau_and_ties_prefer_low_index():
     assert cnt[0] == 4 and idx[0, :4].tolist() == [0, 1, 2, 3]
 
 
+def _unit_masses(row):
+    """Integer masses of a float32 score row (the find_blocks quantisation)."""
+    return [int(np.floor(min(max(float(x), 0.0), 1.0) * 2.0 ** 32)) if x == x else 0
+            for x in row]
+
+
+@pytest.mark.parametrize("ties", [False, True])
+def test_topk_is_the_upper_set_of_the_selection_order(ties):
+    # Top-K (Sec. 4.5, Table 6): exactly min(k, m) blocks, and no unselected
+    # candidate outranks a selected one in the (mass desc, j asc) order; the
+    # two properties determine the set. Output ascending.
+    s, rb = W.random_score_rows(80, 24, seed=21, causal=True, ties=ties)
+    for k in (1, 2, 5, 11, 24, 100):
+        idx, cnt = oracle.select_topk_rows(s, rb, k)
+        for r in range(len(rb)):
+            m = int(rb[r]) + 1
+            sel = idx[r, :cnt[r]].tolist()
+            assert cnt[r] == min(k, m) and sel == sorted(sel) and len(set(sel)) == len(sel)
+            assert all(0 <= j < m for j in sel) and np.all(idx[r, cnt[r]:] == -1)
+            u = _unit_masses(s[r, :m])
+            rest = [j for j in range(m) if j not in sel]
+            for j in sel:
+                for jj in rest:
+                    assert u[j] > u[jj] or (u[j] == u[jj] and j < jj), (r, k, j, jj)
+
+
+def test_topk_sets_nest_and_match_threshold_selection_at_its_count():
+    # Threshold selection is the shortest prefix of the same order, so Top-K
+    # with k = its count returns the same set; larger k only adds blocks.
+    s, rb = W.random_score_rows(150, 40, seed=22, causal=True)
+    for tau in (0.3, 0.8, 0.95):
+        ti, tc = oracle.select_rows(s, rb, tau)
+        ki, kc = oracle.select_topk_rows(s, rb, tc)
+        assert np.array_equal(tc, kc) and np.array_equal(ti, ki)
+    prev = None
+    for k in (1, 3, 8, 20, 40):
+        idx, cnt = oracle.select_topk_rows(s, rb, k)
+        sets = [set(idx[r, :cnt[r]].tolist()) for r in range(len(rb))]
+        if prev is not None:
+            assert all(a <= b for a, b in zip(prev, sets))
+        prev = sets
+
+
+def test_topk_brute_force_mass_is_maximal():
+    # Among all k-subsets of the candidates, the Top-K set has the largest
+    # total integer mass (enumerated on rows of at most 10 candidates).
+    import itertools
+    s, rb = W.random_score_rows(40, 10, seed=23, causal=True)
+    for k in (1, 2, 3, 4):
+        idx, cnt = oracle.select_topk_rows(s, rb, k)
+        for r in range(len(rb)):
+            m = int(rb[r]) + 1
+            u = _unit_masses(s[r, :m])
+            best = max(sum(u[j] for j in c) for c in itertools.combinations(range(m), min(k, m)))
+            assert sum(u[j] for j in idx[r, :cnt[r]]) == best
+
+
+@pytest.mark.parametrize("ratio,m,want", [
+    (0.5, 10, 5), (0.5, 3, 2),          # exact half rounds up
+    (0.27, 100, 27), (0.7, 10, 7),      # fp32 0.27 is above, fp32 0.7 below the decimal
+    (0.31, 16, 5), (0.01, 3, 1),        # 4.96 -> 5; 0.03 -> at least one block
+    (1.0, 9, 9), (2.0, 4, 4),           # everything, never more than the candidates
+])
+def test_ratio_block_count_rounds_to_nearest(ratio, m, want):
+    s = np.zeros((1, m), np.float32)
+    s[0] = np.arange(m, 0, -1) / np.arange(1, m + 1).sum()
+    idx, cnt = oracle.select_ratio_rows(s, np.array([m - 1], np.int32), ratio)
+    assert cnt[0] == want and idx[0, :want].tolist() == list(range(want))
+
+
+def test_per_head_thresholds_apply_each_heads_own_tau():
+    s, rb = W.random_score_rows(120, 32, seed=24, causal=True)
+    rh = np.arange(120) % 6          # 3 query heads x batch 2
+    tau_h = [0.5, 0.9, 0.99]
+    idx, cnt = oracle.select_heads_rows(s, rh, rb, tau_h, hq=3)
+    for hh, tau in enumerate(tau_h):
+        rows = np.nonzero(rh % 3 == hh)[0]
+        i2, c2 = oracle.select_rows(s[rows], rb[rows], tau)
+        assert np.array_equal(idx[rows], i2) and np.array_equal(cnt[rows], c2)
+    assert len({int(c) for c in cnt}) > 1
+
+
 # ---------------------------------------------------------------- attention
 
 
