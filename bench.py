@@ -39,6 +39,16 @@ def parse():
     ap.add_argument("--workload", default="c3", choices=sorted(W.WORKLOADS))
     ap.add_argument("--stride", type=int, default=None)
     ap.add_argument("--tau", type=float, default=None)
+    ap.add_argument("--select-mode", default="threshold",
+                    choices=["threshold", "heads", "topk", "ratio"],
+                    help="block selection: one threshold (default), one threshold per query "
+                         "head (--tau-heads), Top-K (--topk) or Top-Ratio (--ratio)")
+    ap.add_argument("--tau-heads", default="0.8,0.95",
+                    help="per-head thresholds spread linearly from the first to the second "
+                         "value over the query heads")
+    ap.add_argument("--topk", type=int, default=64, help="key blocks per row (Top-K)")
+    ap.add_argument("--ratio", type=float, default=0.05,
+                    help="fraction of each row's candidate blocks (Top-Ratio)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-dense", action="store_true")
     ap.add_argument("--dense-steps", type=int, default=3)
@@ -133,6 +143,18 @@ def main():
     ws = torch.empty(X.score_workspace_size(dims, w.block, w.stride), dtype=torch.uint8,
                      device=dev)
     stream = torch.cuda.current_stream()
+    lo_hi = [float(t) for t in a.tau_heads.split(",")]
+    tau_h = np.linspace(lo_hi[0], lo_hi[-1], w.hq).astype(np.float32)
+
+    def select():
+        if a.select_mode == "threshold":
+            X.xattn_select(scores, dims, w.tau, w.block, idx=idx, cnt=cnt)
+        elif a.select_mode == "heads":
+            X.xattn_select_heads(scores, dims, tau_h, w.block, idx=idx, cnt=cnt)
+        elif a.select_mode == "topk":
+            X.xattn_select_topk(scores, dims, a.topk, w.block, idx=idx, cnt=cnt)
+        else:
+            X.xattn_select_ratio(scores, dims, a.ratio, w.block, idx=idx, cnt=cnt)
 
     def step(ev=None):
         if ev is not None:
@@ -140,7 +162,7 @@ def main():
         X.xattn_score(q, k, w.causal, w.block, w.stride, scores=scores, workspace=ws)
         if ev is not None:
             ev[1].record(stream)
-        X.xattn_select(scores, dims, w.tau, w.block, idx=idx, cnt=cnt)
+        select()
         if ev is not None:
             ev[2].record(stream)
         X.xattn_block_sparse_attn(q, k, v, idx, cnt, w.causal, w.block, o=o, want_lse=False)
@@ -233,7 +255,10 @@ def main():
         "vs_baseline": None,
         "dtype": "bf16",
         "data": "synthetic",
-        "config": w.describe(),
+        "config": dict(w.describe(), **({} if a.select_mode == "threshold" else {
+            "select": {"heads": {"tau_h": [round(float(t), 4) for t in tau_h]},
+                       "topk": {"k_blocks": a.topk},
+                       "ratio": {"ratio": a.ratio}}[a.select_mode] | {"mode": a.select_mode}})),
         "stages_ms": {"score": round(t_score, 4), "select": round(t_select, 4),
                       "attn": round(t_attn, 4)},
         "score_select_share": round((t_score + t_select) / stage_sum, 4),

@@ -102,6 +102,38 @@ int xattn_select(const float *scores, const xattn_dims *dims, int block, float t
                  int32_t *idx, int32_t *cnt, void *stream);
 
 /*
+ * Step 2 with one threshold per query head (the per-head thresholds that the
+ * minimum-threshold prediction of Sec. 3.3 produces). Row (h, b) of batch
+ * element n uses tau_h[h] (rows are indexed n * hq + h); otherwise exactly
+ * xattn_select.
+ *   tau_h  host array of dims->hq floats, each > 0 (values >= 1: all
+ *          candidates); read during the call only (copied into the launch)
+ * Errors: XATTN_ERR_ARG for a NULL array or a tau <= 0 / NaN,
+ * XATTN_ERR_UNSUPPORTED for hq > 256.
+ */
+int xattn_select_heads(const float *scores, const xattn_dims *dims, int block,
+                       const float *tau_h, int32_t *idx, int32_t *cnt, void *stream);
+
+/*
+ * Fixed-size block selection of the selection-strategy ablation (Sec. 4.5,
+ * Table 6: Top-K and Top-Ratio against threshold selection). Per row the
+ * candidates are ordered as in xattn_select, by (u_j descending, j
+ * ascending) with u_j = floor(clamp(score, 0, 1) * 2^32), and the first k are
+ * selected, k clamped to [1, m] for m candidates; output as xattn_select.
+ *   Top-K:     k = k_h[h] key blocks (the paper quotes K in tokens: K tokens
+ *              correspond to K / block blocks); host array of dims->hq
+ *              int32, each >= 1
+ *   Top-Ratio: k = floor(ratio_h[h] * m + 0.5) (fp32 ratio, product in
+ *              fp64), at least 1; host array of dims->hq floats, each finite
+ *              and > 0 (>= 1 keeps every candidate)
+ * The arrays are read during the call only. Errors as xattn_select_heads.
+ */
+int xattn_select_topk(const float *scores, const xattn_dims *dims, int block,
+                      const int32_t *k_h, int32_t *idx, int32_t *cnt, void *stream);
+int xattn_select_ratio(const float *scores, const xattn_dims *dims, int block,
+                       const float *ratio_h, int32_t *idx, int32_t *cnt, void *stream);
+
+/*
  * Step 3 -- block-sparse attention (Fig. 1, right): for query i in block b of
  * head h, with K_i the keys of the listed key blocks idx[h][b][0 .. cnt)
  * (intersected with k <= i when causal):

@@ -16,6 +16,7 @@ from __future__ import annotations
 import ctypes
 import os
 
+import numpy as np
 import torch
 
 from . import build as _build
@@ -55,7 +56,8 @@ class Dims(ctypes.Structure):
 
 
 EXPORTS = [
-    "xattn_score_workspace_size", "xattn_score", "xattn_select", "xattn_block_sparse_attn",
+    "xattn_score_workspace_size", "xattn_score", "xattn_select", "xattn_select_heads",
+    "xattn_select_topk", "xattn_select_ratio", "xattn_block_sparse_attn",
     "xattn_dense_attn", "xattn_forward_workspace_size", "xattn_forward_layout",
     "xattn_forward", "xattn_strerror", "xattn_last_error", "xattn_version",
 ]
@@ -78,6 +80,9 @@ def lib() -> ctypes.CDLL:
         L.xattn_score_workspace_size.argtypes = [PD, I, I, PSZ]
         L.xattn_score.argtypes = [P, P, PD, I, I, P, P, SZ, P]
         L.xattn_select.argtypes = [P, PD, I, F, P, P, P]
+        L.xattn_select_heads.argtypes = [P, PD, I, P, P, P, P]
+        L.xattn_select_topk.argtypes = [P, PD, I, P, P, P, P]
+        L.xattn_select_ratio.argtypes = [P, PD, I, P, P, P, P]
         L.xattn_block_sparse_attn.argtypes = [P, P, P, PD, I, P, P, P, P, P]
         L.xattn_dense_attn.argtypes = [P, P, P, PD, P, P, P]
         L.xattn_forward_workspace_size.argtypes = [PD, I, I, PSZ]
@@ -181,6 +186,53 @@ def xattn_select(scores, dims: Dims, tau: float, block=BLOCK, idx=None, cnt=None
     _need(cnt, torch.int32, "cnt")
     _check(lib().xattn_select(_ptr(scores), ctypes.byref(dims), block, float(tau), _ptr(idx),
                               _ptr(cnt), _stream(stream)))
+    return idx, cnt
+
+
+def _select_outputs(scores, dims, block, idx, cnt):
+    _need(scores, torch.float32, "scores")
+    nb = dims.seq // block
+    if idx is None:
+        idx = torch.full((dims.heads, nb, nb), -1, dtype=torch.int32, device=scores.device)
+    if cnt is None:
+        cnt = torch.empty((dims.heads, nb), dtype=torch.int32, device=scores.device)
+    _need(idx, torch.int32, "idx")
+    _need(cnt, torch.int32, "cnt")
+    return idx, cnt
+
+
+def _per_head(values, dims, dtype):
+    """Host array of dims.hq values (a scalar is repeated for every head)."""
+    a = np.ascontiguousarray(np.broadcast_to(np.asarray(values, dtype=dtype), (dims.hq,)))
+    return a, a.ctypes.data_as(ctypes.c_void_p)
+
+
+def xattn_select_heads(scores, dims: Dims, tau_h, block=BLOCK, idx=None, cnt=None,
+                       stream=None):
+    """find_blocks with one threshold per query head (tau_h: dims.hq values)."""
+    idx, cnt = _select_outputs(scores, dims, block, idx, cnt)
+    a, p = _per_head(tau_h, dims, np.float32)
+    _check(lib().xattn_select_heads(_ptr(scores), ctypes.byref(dims), block, p, _ptr(idx),
+                                    _ptr(cnt), _stream(stream)))
+    return idx, cnt
+
+
+def xattn_select_topk(scores, dims: Dims, k_h, block=BLOCK, idx=None, cnt=None, stream=None):
+    """Top-K key blocks per row (k_h: dims.hq block counts, or one for all heads)."""
+    idx, cnt = _select_outputs(scores, dims, block, idx, cnt)
+    a, p = _per_head(k_h, dims, np.int32)
+    _check(lib().xattn_select_topk(_ptr(scores), ctypes.byref(dims), block, p, _ptr(idx),
+                                   _ptr(cnt), _stream(stream)))
+    return idx, cnt
+
+
+def xattn_select_ratio(scores, dims: Dims, ratio_h, block=BLOCK, idx=None, cnt=None,
+                       stream=None):
+    """Top-Ratio: round(ratio * candidates) key blocks per row (at least one)."""
+    idx, cnt = _select_outputs(scores, dims, block, idx, cnt)
+    a, p = _per_head(ratio_h, dims, np.float32)
+    _check(lib().xattn_select_ratio(_ptr(scores), ctypes.byref(dims), block, p, _ptr(idx),
+                                    _ptr(cnt), _stream(stream)))
     return idx, cnt
 
 

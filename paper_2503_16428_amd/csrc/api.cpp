@@ -79,6 +79,31 @@ int hip_status(hipError_t e, const char* what) {
   return ok();
 }
 
+SelectParams uniform_threshold(const XattnShape& s, float tau) {
+  SelectParams p{};
+  p.mode = kSelectThreshold;
+  p.hq = s.hq;
+  p.uniform = 1;
+  p.v[0] = tau;
+  return p;
+}
+
+SelectParams per_head(const XattnShape& s, int mode) {
+  SelectParams p{};
+  p.mode = mode;
+  p.hq = s.hq;
+  p.uniform = 0;
+  return p;
+}
+
+int check_heads(const XattnShape& s, const void* values) {
+  if (!values) return fail(XATTN_ERR_ARG, "the per-head parameter array is NULL");
+  if (s.hq > kMaxSelectHeads)
+    return fail(XATTN_ERR_UNSUPPORTED, "per-head selection supports hq <= %d (got %d)",
+                kMaxSelectHeads, s.hq);
+  return XATTN_OK;
+}
+
 size_t scores_bytes(const XattnShape& s) { return (size_t)s.HQ() * s.NB() * s.NB() * 4; }
 size_t idx_bytes(const XattnShape& s) { return (size_t)s.HQ() * s.NB() * s.NB() * 4; }
 size_t cnt_bytes(const XattnShape& s) { return (size_t)s.HQ() * s.NB() * 4; }
@@ -119,8 +144,60 @@ int xattn_select(const float* scores, const xattn_dims* dims, int block, float t
   if ((rc = check_dims(dims, &s)) || (rc = check_block(block)) || (rc = check_tau(tau)))
     return rc;
   if (!scores || !idx || !cnt) return fail(XATTN_ERR_ARG, "scores, idx and cnt must be non-NULL");
-  return hip_status(launch_select(scores, s, tau, idx, cnt, (hipStream_t)stream),
+  return hip_status(launch_select(scores, s, uniform_threshold(s, tau), idx, cnt,
+                                  (hipStream_t)stream),
                     "xattn_select launch");
+}
+
+int xattn_select_heads(const float* scores, const xattn_dims* dims, int block,
+                       const float* tau_h, int32_t* idx, int32_t* cnt, void* stream) {
+  XattnShape s;
+  int rc;
+  if ((rc = check_dims(dims, &s)) || (rc = check_block(block)) || (rc = check_heads(s, tau_h)))
+    return rc;
+  SelectParams p = per_head(s, kSelectThreshold);
+  for (int i = 0; i < s.hq; ++i) {
+    if (!(tau_h[i] > 0.f))
+      return fail(XATTN_ERR_ARG, "tau_h[%d] must be > 0 (got %g)", i, (double)tau_h[i]);
+    p.v[i] = tau_h[i];
+  }
+  if (!scores || !idx || !cnt) return fail(XATTN_ERR_ARG, "scores, idx and cnt must be non-NULL");
+  return hip_status(launch_select(scores, s, p, idx, cnt, (hipStream_t)stream),
+                    "xattn_select_heads launch");
+}
+
+int xattn_select_topk(const float* scores, const xattn_dims* dims, int block,
+                      const int32_t* k_h, int32_t* idx, int32_t* cnt, void* stream) {
+  XattnShape s;
+  int rc;
+  if ((rc = check_dims(dims, &s)) || (rc = check_block(block)) || (rc = check_heads(s, k_h)))
+    return rc;
+  SelectParams p = per_head(s, kSelectTopK);
+  for (int i = 0; i < s.hq; ++i) {
+    if (k_h[i] < 1) return fail(XATTN_ERR_ARG, "k_h[%d] must be >= 1 (got %d)", i, k_h[i]);
+    p.k[i] = k_h[i];
+  }
+  if (!scores || !idx || !cnt) return fail(XATTN_ERR_ARG, "scores, idx and cnt must be non-NULL");
+  return hip_status(launch_select(scores, s, p, idx, cnt, (hipStream_t)stream),
+                    "xattn_select_topk launch");
+}
+
+int xattn_select_ratio(const float* scores, const xattn_dims* dims, int block,
+                       const float* ratio_h, int32_t* idx, int32_t* cnt, void* stream) {
+  XattnShape s;
+  int rc;
+  if ((rc = check_dims(dims, &s)) || (rc = check_block(block)) || (rc = check_heads(s, ratio_h)))
+    return rc;
+  SelectParams p = per_head(s, kSelectRatio);
+  for (int i = 0; i < s.hq; ++i) {
+    const float r = ratio_h[i];
+    if (!(r > 0.f) || !std::isfinite(r))
+      return fail(XATTN_ERR_ARG, "ratio_h[%d] must be finite and > 0 (got %g)", i, (double)r);
+    p.v[i] = r;
+  }
+  if (!scores || !idx || !cnt) return fail(XATTN_ERR_ARG, "scores, idx and cnt must be non-NULL");
+  return hip_status(launch_select(scores, s, p, idx, cnt, (hipStream_t)stream),
+                    "xattn_select_ratio launch");
 }
 
 int xattn_block_sparse_attn(const void* q, const void* k, const void* v, const xattn_dims* dims,
@@ -194,7 +271,7 @@ int xattn_forward(const void* q, const void* k, const void* v, const xattn_dims*
   int32_t* cnt = (int32_t*)(ws + o_cnt);
   hipStream_t st = (hipStream_t)stream;
   hipError_t e = launch_score(q, k, s, stride, sc, ws + o_scr, st);
-  if (e == hipSuccess) e = launch_select(sc, s, tau, idx, cnt, st);
+  if (e == hipSuccess) e = launch_select(sc, s, uniform_threshold(s, tau), idx, cnt, st);
   if (e == hipSuccess) e = launch_attn(q, k, v, s, idx, cnt, false, o, lse, st);
   return hip_status(e, "xattn_forward launch");
 }

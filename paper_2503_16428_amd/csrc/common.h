@@ -91,8 +91,19 @@ struct XattnShape {
 hipError_t launch_score(const void* q, const void* k, const XattnShape& s, int stride,
                         float* scores, void* scratch, hipStream_t st);
 size_t score_scratch_bytes(const XattnShape& s, int stride);
-hipError_t launch_select(const float* scores, const XattnShape& s, float tau, int32_t* idx,
-                         int32_t* cnt, hipStream_t st);
+// Selection rule of one launch: find_blocks with a threshold per head, or a
+// fixed block count per head (Top-K) or fraction of the candidates
+// (Top-Ratio). Passed by value as a kernel argument; with uniform != 0 every
+// head uses entry 0 (then hq may exceed kMaxSelectHeads).
+constexpr int kMaxSelectHeads = 256;
+enum { kSelectThreshold = 0, kSelectTopK = 1, kSelectRatio = 2 };
+struct SelectParams {
+  int mode, hq, uniform;
+  float v[kMaxSelectHeads];  // tau (threshold) or ratio (Top-Ratio)
+  int k[kMaxSelectHeads];    // blocks (Top-K)
+};
+hipError_t launch_select(const float* scores, const XattnShape& s, const SelectParams& p,
+                         int32_t* idx, int32_t* cnt, hipStream_t st);
 hipError_t launch_attn(const void* q, const void* k, const void* v, const XattnShape& s,
                        const int32_t* idx, const int32_t* cnt, bool dense, void* o,
                        float* lse, hipStream_t st);

@@ -5,6 +5,10 @@
 // below is exact and the result does not depend on summation order; the
 // target is ceil(tau * T) with T the row total (one fp64 product).
 //
+// The same search serves the fixed-size selections of the Top-K / Top-Ratio
+// ablation (Sec. 4.5, Table 6) with block counts instead of masses, and
+// thresholds may differ per head (the consumer side of Sec. 3.3).
+//
 // One wave64 per (head, query block) row. Instead of sorting, the wave finds
 // the mass v* of the last block the sorted prefix needs: the largest v with
 // F(v) = sum_{u_j >= v} u_j >= target (binary search, F non-increasing).
@@ -39,9 +43,13 @@ __device__ __forceinline__ uint64_t wave_sum_u64(uint64_t x) {
 
 // One row with at most 64 NPL candidates; lane l holds j = l + 64 i. Every
 // per-lane partial sum below is at most NPL * 2^32 <= 2^37.
-template <int NPL>
+//   COUNT = false (find_blocks): target = ceil(tau * T), F(v) = sum_{u >= v} u.
+//   COUNT = true (Top-K / Top-Ratio): target = k, F(v) = #{u >= v}.
+// v* = the largest v with F(v) >= target; the selection is every u > v* plus
+// the first ties (u == v*) in ascending j that bring it to the target.
+template <int NPL, bool COUNT>
 __device__ __forceinline__ void select_row(const float* __restrict__ s, int m, float tau,
-                                           int lane, int32_t* __restrict__ out,
+                                           int k, int lane, int32_t* __restrict__ out,
                                            int32_t* __restrict__ cnt_out) {
   uint64_t u[NPL];
   uint64_t tl = 0;
@@ -53,33 +61,42 @@ __device__ __forceinline__ void select_row(const float* __restrict__ s, int m, f
     u[i] = (uint64_t)floor((double)v * 4294967296.0);
     tl += u[i];
   }
-  const uint64_t T = wave_sum_u64(tl);
-  if (T == 0) {  // every candidate has zero mass: the first in (u desc, j asc) order is j = 0
-    if (lane == 0) {
-      out[0] = 0;
-      *cnt_out = 1;
+  uint64_t target;
+  if constexpr (COUNT) {
+    target = (uint64_t)k;  // 1 <= k < m
+  } else {
+    const uint64_t T = wave_sum_u64(tl);
+    if (T == 0) {  // every candidate has zero mass: the first in (u desc, j asc) order is j = 0
+      if (lane == 0) {
+        out[0] = 0;
+        *cnt_out = 1;
+      }
+      return;
     }
-    return;
+    const double prod = (double)tau * (double)T;
+    target = (uint64_t)ceil(prod);
   }
-  const double prod = (double)tau * (double)T;
-  const uint64_t target = (uint64_t)ceil(prod);
+  auto F = [&](uint64_t v, bool strict) -> uint64_t {
+    uint64_t f = 0;
+#pragma unroll
+    for (int i = 0; i < NPL; ++i) {
+      const bool in = strict ? u[i] > v : u[i] >= v;
+      f += in ? (COUNT ? 1 : u[i]) : 0;
+    }
+    return wave_sum_u64(f);
+  };
 
-  // largest v in [0, 2^32] with F(v) >= target; F(0) = T >= target, F(2^32 + 1) = 0
+  // largest v in [0, 2^32] with F(v) >= target; F(0) >= target, F(2^32 + 1) = 0
   uint64_t lo = 0, hi = (1ull << 32) + 1;
   while (hi - lo > 1) {
     const uint64_t mid = (lo + hi) >> 1;
-    uint64_t f = 0;
-#pragma unroll
-    for (int i = 0; i < NPL; ++i) f += u[i] >= mid ? u[i] : 0;
-    if (wave_sum_u64(f) >= target) lo = mid;
+    if (F(mid, false) >= target) lo = mid;
     else hi = mid;
   }
-  const uint64_t vstar = lo;  // >= 1 because F(1) = T >= target
-  uint64_t bl = 0;
-#pragma unroll
-  for (int i = 0; i < NPL; ++i) bl += u[i] > vstar ? u[i] : 0;
-  const uint64_t base = wave_sum_u64(bl);  // < target by maximality of v*
-  const uint64_t ties_needed = (target - base + vstar - 1) / vstar;
+  const uint64_t vstar = lo;
+  const uint64_t base = F(vstar, true);  // < target by maximality of v*
+  // find_blocks: v* >= 1 because F(1) = T >= target
+  const uint64_t ties_needed = COUNT ? target - base : (target - base + vstar - 1) / vstar;
 
   const uint64_t below = (1ull << lane) - 1ull;
   uint32_t written = 0;
@@ -99,60 +116,78 @@ __device__ __forceinline__ void select_row(const float* __restrict__ s, int m, f
   if (lane == 0) *cnt_out = (int32_t)written;
 }
 
+template <int NPL, bool COUNT>
+__device__ __forceinline__ void select_row_sized(const float* s, int m, float tau, int k,
+                                                 int lane, int32_t* out, int32_t* cnt_out) {
+  const int nact = (m + 63) >> 6;
+  if (NPL <= 1 || nact <= 1) select_row<1, COUNT>(s, m, tau, k, lane, out, cnt_out);
+  else if (NPL <= 2 || nact <= 2) select_row<(NPL < 2 ? NPL : 2), COUNT>(s, m, tau, k, lane, out, cnt_out);
+  else if (NPL <= 4 || nact <= 4) select_row<(NPL < 4 ? NPL : 4), COUNT>(s, m, tau, k, lane, out, cnt_out);
+  else if (NPL <= 8 || nact <= 8) select_row<(NPL < 8 ? NPL : 8), COUNT>(s, m, tau, k, lane, out, cnt_out);
+  else if (NPL <= 16 || nact <= 16) select_row<(NPL < 16 ? NPL : 16), COUNT>(s, m, tau, k, lane, out, cnt_out);
+  else select_row<NPL, COUNT>(s, m, tau, k, lane, out, cnt_out);
+}
+
 // One wave64 per (head, query block) row. NPL = slots per lane for the
 // longest row (64 NPL >= NB); a causal row with m = b + 1 candidates runs the
-// smallest power-of-two slot count that holds them.
+// smallest power-of-two slot count that holds them. Per-head parameters are
+// indexed by the row's head modulo hq (the same for every batch element).
 template <int NPL, bool CAUSAL>
 __global__ __launch_bounds__(256) void select_kernel(const float* __restrict__ scores,
-                                                     int n_rows, int NB, float tau,
+                                                     int n_rows, int NB, SelectParams p,
                                                      int32_t* __restrict__ idx,
                                                      int32_t* __restrict__ cnt) {
   const int lane = threadIdx.x & 63;
   const int row = blockIdx.x * 4 + (threadIdx.x >> 6);
   if (row >= n_rows) return;  // uniform per wave
   const int b = row % NB;
+  const int hp = p.uniform ? 0 : (row / NB) % p.hq;
   const int m = CAUSAL ? b + 1 : NB;
   const float* s = scores + (size_t)row * NB;
   int32_t* out = idx + (size_t)row * NB;
 
-  if (tau >= 1.f) {
+  int k = m;  // blocks a fixed-size mode keeps
+  if (p.mode == kSelectTopK) {
+    k = p.k[hp];
+  } else if (p.mode == kSelectRatio) {
+    const double want = floor((double)p.v[hp] * (double)m + 0.5);
+    k = want < 1.0 ? 1 : (want > (double)m ? m : (int)want);
+  }
+  k = k < 1 ? 1 : k;
+  const bool all = p.mode == kSelectThreshold ? p.v[hp] >= 1.f : k >= m;
+  if (all) {
     for (int j = lane; j < m; j += 64) out[j] = j;
     if (lane == 0) cnt[row] = m;
     return;
   }
-  const int nact = (m + 63) >> 6;
-  if (NPL <= 1 || nact <= 1) select_row<1>(s, m, tau, lane, out, cnt + row);
-  else if (NPL <= 2 || nact <= 2) select_row<(NPL < 2 ? NPL : 2)>(s, m, tau, lane, out, cnt + row);
-  else if (NPL <= 4 || nact <= 4) select_row<(NPL < 4 ? NPL : 4)>(s, m, tau, lane, out, cnt + row);
-  else if (NPL <= 8 || nact <= 8) select_row<(NPL < 8 ? NPL : 8)>(s, m, tau, lane, out, cnt + row);
-  else if (NPL <= 16 || nact <= 16) select_row<(NPL < 16 ? NPL : 16)>(s, m, tau, lane, out, cnt + row);
-  else select_row<NPL>(s, m, tau, lane, out, cnt + row);
+  if (p.mode == kSelectThreshold) select_row_sized<NPL, false>(s, m, p.v[hp], 0, lane, out, cnt + row);
+  else select_row_sized<NPL, true>(s, m, 0.f, k, lane, out, cnt + row);
 }
 
 template <int NPL>
-hipError_t launch_npl(const float* scores, const XattnShape& s, float tau, int32_t* idx,
-                      int32_t* cnt, hipStream_t st) {
+hipError_t launch_npl(const float* scores, const XattnShape& s, const SelectParams& p,
+                      int32_t* idx, int32_t* cnt, hipStream_t st) {
   const int n_rows = s.HQ() * s.NB();
   const dim3 grid((n_rows + 3) / 4);
   if (s.causal)
     hipLaunchKernelGGL((select_kernel<NPL, true>), grid, dim3(256), 0, st, scores, n_rows,
-                       s.NB(), tau, idx, cnt);
+                       s.NB(), p, idx, cnt);
   else
     hipLaunchKernelGGL((select_kernel<NPL, false>), grid, dim3(256), 0, st, scores, n_rows,
-                       s.NB(), tau, idx, cnt);
+                       s.NB(), p, idx, cnt);
   return hipGetLastError();
 }
 
 }  // namespace
 
-hipError_t launch_select(const float* scores, const XattnShape& s, float tau, int32_t* idx,
-                         int32_t* cnt, hipStream_t st) {
+hipError_t launch_select(const float* scores, const XattnShape& s, const SelectParams& p,
+                         int32_t* idx, int32_t* cnt, hipStream_t st) {
   const int NB = s.NB();
-  if (NB <= 64) return launch_npl<1>(scores, s, tau, idx, cnt, st);
-  if (NB <= 128) return launch_npl<2>(scores, s, tau, idx, cnt, st);
-  if (NB <= 256) return launch_npl<4>(scores, s, tau, idx, cnt, st);
-  if (NB <= 512) return launch_npl<8>(scores, s, tau, idx, cnt, st);
-  if (NB <= 1024) return launch_npl<16>(scores, s, tau, idx, cnt, st);
-  if (NB <= 2048) return launch_npl<32>(scores, s, tau, idx, cnt, st);
+  if (NB <= 64) return launch_npl<1>(scores, s, p, idx, cnt, st);
+  if (NB <= 128) return launch_npl<2>(scores, s, p, idx, cnt, st);
+  if (NB <= 256) return launch_npl<4>(scores, s, p, idx, cnt, st);
+  if (NB <= 512) return launch_npl<8>(scores, s, p, idx, cnt, st);
+  if (NB <= 1024) return launch_npl<16>(scores, s, p, idx, cnt, st);
+  if (NB <= 2048) return launch_npl<32>(scores, s, p, idx, cnt, st);
   return hipErrorInvalidValue;
 }

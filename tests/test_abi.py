@@ -111,3 +111,32 @@ def test_calls_validate_before_launch():
                            None) == B.XATTN_ERR_WORKSPACE
     assert L.xattn_dense_attn(fake, fake, fake, None, fake, None, None) == B.XATTN_ERR_ARG
     assert L.xattn_strerror(99) == b"unknown status"
+
+
+def test_per_head_selection_validates_before_launch():
+    L = X.lib()
+    d = _dims()                      # hq = 4
+    fake = ctypes.c_void_p(0x1000)   # never dereferenced: every case fails validation
+
+    def arr(vals, ct):
+        a = (ct * len(vals))(*vals)
+        return ctypes.cast(a, ctypes.c_void_p), a
+
+    for fn, ct, bad in ((L.xattn_select_heads, ctypes.c_float, [0.9, 0.9, 0.0, 0.9]),
+                        (L.xattn_select_heads, ctypes.c_float, [0.9, float("nan"), 0.9, 0.9]),
+                        (L.xattn_select_topk, ctypes.c_int32, [4, 0, 4, 4]),
+                        (L.xattn_select_topk, ctypes.c_int32, [4, 4, 4, -3]),
+                        (L.xattn_select_ratio, ctypes.c_float, [0.3, 0.3, -0.1, 0.3]),
+                        (L.xattn_select_ratio, ctypes.c_float, [float("inf"), 0.3, 0.3, 0.3])):
+        p, keep = arr(bad, ct)
+        assert fn(fake, ctypes.byref(d), 128, p, fake, fake, None) == B.XATTN_ERR_ARG
+        assert b"[" in L.xattn_last_error()          # names the offending head
+    for fn in (L.xattn_select_heads, L.xattn_select_topk, L.xattn_select_ratio):
+        assert fn(fake, ctypes.byref(d), 128, None, fake, fake, None) == B.XATTN_ERR_ARG
+    big = _dims(hq=512, hkv=512)
+    p, keep = arr([0.5] * 512, ctypes.c_float)
+    assert L.xattn_select_heads(fake, ctypes.byref(big), 128, p, fake, fake, None) == \
+        B.XATTN_ERR_UNSUPPORTED
+    p, keep = arr([0.5] * 4, ctypes.c_float)
+    assert L.xattn_select_ratio(None, ctypes.byref(d), 128, p, fake, fake, None) == \
+        B.XATTN_ERR_ARG
