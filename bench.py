@@ -36,7 +36,8 @@ def parse():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=3)
-    ap.add_argument("--workload", default="c3", choices=sorted(W.WORKLOADS))
+    ap.add_argument("--workload", default=None, choices=sorted(W.WORKLOADS),
+                    help="default c3 (c5 with --dit-schedule)")
     ap.add_argument("--stride", type=int, default=None)
     ap.add_argument("--tau", type=float, default=None)
     ap.add_argument("--select-mode", default="threshold",
@@ -49,6 +50,10 @@ def parse():
     ap.add_argument("--topk", type=int, default=64, help="key blocks per row (Top-K)")
     ap.add_argument("--ratio", type=float, default=0.05,
                     help="fraction of each row's candidate blocks (Top-Ratio)")
+    ap.add_argument("--dit-schedule", default=None, metavar="T,W",
+                    help="video-DiT denoising schedule: time T layer steps (step t uses "
+                         "dense attention for t < W, XAttention afterwards); default "
+                         "workload c5")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-dense", action="store_true")
     ap.add_argument("--dense-steps", type=int, default=3)
@@ -114,6 +119,56 @@ def read_traffic(path, w, kernel):
     return None
 
 
+def schedule_main(a, w, q, k, v, dims, stream):
+    """One video-DiT denoising run per T steps: layer step t runs dense
+    attention for t < W and score -> select -> sparse attention afterwards
+    (xattn_forward_scheduled). Warmup steps replay the schedule untimed."""
+    import torch
+    import paper_2503_16428_amd as X
+    T, Wm = (int(t) for t in a.dit_schedule.split(","))
+    o = torch.empty_like(q)
+    ws = torch.empty(X.forward_workspace_size(dims, w.block, w.stride), dtype=torch.uint8,
+                     device=q.device)
+
+    def step(t):
+        X.xattn_forward_scheduled(q, k, v, t % T, warmup_steps=Wm, causal=w.causal,
+                                  block=w.block, stride=w.stride, tau=w.tau, o=o, workspace=ws)
+
+    for i in range(a.warmup):
+        step(i)
+    torch.cuda.synchronize()
+    evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+           for _ in range(a.steps)]
+    t0 = time.perf_counter()
+    for i in range(a.steps):
+        evs[i][0].record(stream)
+        step(i)
+        evs[i][1].record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    per = np.array([e[0].elapsed_time(e[1]) for e in evs])
+    is_dense = np.array([(i % T) < Wm for i in range(a.steps)])
+    ms_step = wall * 1e3 / a.steps
+    dense_ms = float(per[is_dense].mean()) if is_dense.any() else None
+    sparse_ms = float(per[~is_dense].mean()) if (~is_dense).any() else None
+    value = dense_flops(w) / (ms_step * 1e-3) / 1e12
+    out = {
+        "metric": "ms per denoising-step layer + dense-equiv TFLOP/s under the video-DiT "
+                  "warm-up schedule",
+        "value": round(value, 3), "unit": "TFLOP/s (dense-equivalent)",
+        "n_gpus": 1, "steps": a.steps, "warmup": a.warmup, "ms_per_step": round(ms_step, 4),
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "bf16",
+        "data": "synthetic",
+        "config": dict(w.describe(), schedule={"denoising_steps": T, "dense_warmup": Wm}),
+        "dense_step_ms": None if dense_ms is None else round(dense_ms, 4),
+        "xattn_step_ms": None if sparse_ms is None else round(sparse_ms, 4),
+        "speedup_vs_all_dense": (None if dense_ms is None else
+                                 round(dense_ms / float(per.mean()), 3)),
+        "roofline": None, "cpu_baseline": None,
+    }
+    print(json.dumps(out), flush=True)
+
+
 def main():
     a = parse()
     if a.gpus != 1:
@@ -123,7 +178,7 @@ def main():
     import torch
     import paper_2503_16428_amd as X
 
-    w = W.WORKLOADS[a.workload]
+    w = W.WORKLOADS[a.workload or ("c5" if a.dit_schedule else "c3")]
     if a.stride is not None:
         w = w.with_(stride=a.stride)
     if a.tau is not None:
@@ -143,6 +198,9 @@ def main():
     ws = torch.empty(X.score_workspace_size(dims, w.block, w.stride), dtype=torch.uint8,
                      device=dev)
     stream = torch.cuda.current_stream()
+    if a.dit_schedule:
+        schedule_main(a, w, q, k, v, dims, stream)
+        return
     lo_hi = [float(t) for t in a.tau_heads.split(",")]
     tau_h = np.linspace(lo_hi[0], lo_hi[-1], w.hq).astype(np.float32)
 

@@ -177,6 +177,20 @@ int xattn_forward(const void *q, const void *k, const void *v, const xattn_dims 
                   int block, int stride, float tau, void *o, float *lse,
                   void *workspace, size_t workspace_bytes, void *stream);
 
+/*
+ * Denoising-step schedule of the video-generation experiment (Sec. 4.2):
+ * dense attention for the first warmup_steps steps of a diffusion sampler
+ * (step < warmup_steps; the paper uses 5 of 50), XAttention from then on.
+ *   step          0-based index of the current denoising step (>= 0)
+ *   warmup_steps  number of leading dense steps (>= 0; 0 = never dense)
+ * A dense step is exactly xattn_dense_attn (the workspace is not touched and
+ * may be NULL); a later step is exactly xattn_forward with the same arguments.
+ */
+int xattn_forward_scheduled(const void *q, const void *k, const void *v,
+                            const xattn_dims *dims, int block, int stride, float tau,
+                            int step, int warmup_steps, void *o, float *lse,
+                            void *workspace, size_t workspace_bytes, void *stream);
+
 /* Static description of a status code (never NULL). */
 const char *xattn_strerror(int status);
 /* Message describing the last failure on the calling thread ("" if none). */

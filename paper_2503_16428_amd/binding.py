@@ -59,7 +59,8 @@ EXPORTS = [
     "xattn_score_workspace_size", "xattn_score", "xattn_select", "xattn_select_heads",
     "xattn_select_topk", "xattn_select_ratio", "xattn_block_sparse_attn",
     "xattn_dense_attn", "xattn_forward_workspace_size", "xattn_forward_layout",
-    "xattn_forward", "xattn_strerror", "xattn_last_error", "xattn_version",
+    "xattn_forward", "xattn_forward_scheduled", "xattn_strerror", "xattn_last_error",
+    "xattn_version",
 ]
 
 
@@ -88,6 +89,7 @@ def lib() -> ctypes.CDLL:
         L.xattn_forward_workspace_size.argtypes = [PD, I, I, PSZ]
         L.xattn_forward_layout.argtypes = [PD, I, I, PSZ, PSZ, PSZ, PSZ]
         L.xattn_forward.argtypes = [P, P, P, PD, I, I, F, P, P, P, SZ, P]
+        L.xattn_forward_scheduled.argtypes = [P, P, P, PD, I, I, F, I, I, P, P, P, SZ, P]
         L.xattn_strerror.argtypes = [I]
         L.xattn_strerror.restype = ctypes.c_char_p
         L.xattn_last_error.restype = ctypes.c_char_p
@@ -295,6 +297,29 @@ def xattn_forward(q, k, v, causal=True, block=BLOCK, stride=8, tau=0.9, o=None, 
         .view(torch.int32).view(d.heads, nb),
     }
     return o, lse, views
+
+
+def xattn_forward_scheduled(q, k, v, step, warmup_steps=5, causal=False, block=BLOCK,
+                            stride=16, tau=0.9, o=None, lse=None, workspace=None,
+                            want_lse=False, stream=None):
+    """Dense attention for steps < warmup_steps, XAttention afterwards (video
+    DiT schedule). Returns (o, lse); the workspace is allocated only when needed."""
+    for t, n in ((q, "q"), (k, "k"), (v, "v")):
+        _need(t, torch.bfloat16, n)
+    d = make_dims(q, k, causal)
+    if workspace is None and step >= warmup_steps:
+        workspace = torch.empty(forward_workspace_size(d, block, stride), dtype=torch.uint8,
+                                device=q.device)
+    if o is None:
+        o = torch.empty_like(q)
+    if lse is None and want_lse:
+        lse = torch.empty((d.heads, d.seq), dtype=torch.float32, device=q.device)
+    _check(lib().xattn_forward_scheduled(_ptr(q), _ptr(k), _ptr(v), ctypes.byref(d), block,
+                                         stride, float(tau), int(step), int(warmup_steps),
+                                         _ptr(o), _ptr(lse), _ptr(workspace),
+                                         0 if workspace is None else workspace.numel(),
+                                         _stream(stream)))
+    return o, lse
 
 
 def version() -> int:

@@ -276,6 +276,25 @@ int xattn_forward(const void* q, const void* k, const void* v, const xattn_dims*
   return hip_status(e, "xattn_forward launch");
 }
 
+int xattn_forward_scheduled(const void* q, const void* k, const void* v, const xattn_dims* dims,
+                            int block, int stride, float tau, int step, int warmup_steps,
+                            void* o, float* lse, void* workspace, size_t workspace_bytes,
+                            void* stream) {
+  if (step < 0) return fail(XATTN_ERR_ARG, "step must be >= 0 (got %d)", step);
+  if (warmup_steps < 0)
+    return fail(XATTN_ERR_ARG, "warmup_steps must be >= 0 (got %d)", warmup_steps);
+  if (step < warmup_steps) {
+    XattnShape s;
+    int rc;
+    if ((rc = check_dims(dims, &s)) || (rc = check_block(block)) || (rc = check_stride(stride)) ||
+        (rc = check_tau(tau)))
+      return rc;
+    return xattn_dense_attn(q, k, v, dims, o, lse, stream);
+  }
+  return xattn_forward(q, k, v, dims, block, stride, tau, o, lse, workspace, workspace_bytes,
+                       stream);
+}
+
 const char* xattn_strerror(int status) {
   switch (status) {
     case XATTN_OK: return "ok";

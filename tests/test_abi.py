@@ -140,3 +140,23 @@ def test_per_head_selection_validates_before_launch():
     p, keep = arr([0.5] * 4, ctypes.c_float)
     assert L.xattn_select_ratio(None, ctypes.byref(d), 128, p, fake, fake, None) == \
         B.XATTN_ERR_ARG
+
+
+def test_scheduled_forward_validates_before_launch():
+    L = X.lib()
+    d = _dims()
+    fake = ctypes.c_void_p(0x1000)   # never dereferenced: every case fails validation
+    assert L.xattn_forward_scheduled(fake, fake, fake, ctypes.byref(d), 128, 8, 0.9, -1, 5,
+                                     fake, None, None, 0, None) == B.XATTN_ERR_ARG
+    assert L.xattn_forward_scheduled(fake, fake, fake, ctypes.byref(d), 128, 8, 0.9, 0, -2,
+                                     fake, None, None, 0, None) == B.XATTN_ERR_ARG
+    # a dense step still checks every argument of the later sparse steps
+    assert L.xattn_forward_scheduled(fake, fake, fake, ctypes.byref(d), 128, 3, 0.9, 0, 5,
+                                     fake, None, None, 0, None) == B.XATTN_ERR_ARG
+    assert L.xattn_forward_scheduled(fake, fake, fake, ctypes.byref(d), 128, 8, 0.0, 0, 5,
+                                     fake, None, None, 0, None) == B.XATTN_ERR_ARG
+    assert L.xattn_forward_scheduled(fake, fake, None, ctypes.byref(d), 128, 8, 0.9, 0, 5,
+                                     fake, None, None, 0, None) == B.XATTN_ERR_ARG
+    # a sparse step needs the workspace
+    assert L.xattn_forward_scheduled(fake, fake, fake, ctypes.byref(d), 128, 8, 0.9, 5, 5,
+                                     fake, None, None, 0, None) == B.XATTN_ERR_WORKSPACE
