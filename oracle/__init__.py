@@ -51,6 +51,7 @@ def lib():
         L.oracle_score_rows.argtypes = [P, P, P, i, i, i, P, P, P]
         L.oracle_select_rows.argtypes = [P, i, i, i, P, ctypes.c_float, P, P]
         L.oracle_select_topk_rows.argtypes = [P, i, i, i, P, P, P, P]
+        L.oracle_score_pattern_rows.argtypes = [P, P, P, i, i, P, i, P, P, P]
         L.oracle_select_ratio_rows.argtypes = [P, i, i, i, P, P, P, P]
         L.oracle_sparse_attn_rows.argtypes = [P, P, P, P, i, i, P, P, P, i, P, P, P]
         L.oracle_dense_attn_rows.argtypes = [P, P, P, P, i, i, P, P, P, P]
@@ -101,6 +102,21 @@ def score_rows(q, k, B, S, causal=True, rows=None, batch=1):
     out = np.zeros((len(rh), d.seq // B), dtype=np.float64)
     lib().oracle_score_rows(_ptr(q), _ptr(k), ctypes.byref(d), B, S, len(rh),
                             _ptr(rh), _ptr(rb), _ptr(out))
+    return out
+
+
+def score_pattern_rows(q, k, B, S, qsub, causal=True, rows=None, batch=1):
+    """Block scores with the sub-block positions (qsub[t], t) instead of the
+    antidiagonal (qsub = S-1-t reproduces score_rows)."""
+    q, k = _u16(q), _u16(k)
+    d = _dims(q, k, causal, batch)
+    assert d.seq % B == 0 and B % S == 0
+    qs = np.ascontiguousarray(qsub, dtype=np.int32)
+    assert sorted(qs.tolist()) == list(range(S)), "qsub must be a permutation of 0..S-1"
+    rh, rb = _rows(rows, q, B)
+    out = np.zeros((len(rh), d.seq // B), dtype=np.float64)
+    lib().oracle_score_pattern_rows(_ptr(q), _ptr(k), ctypes.byref(d), B, S, _ptr(qs),
+                                    len(rh), _ptr(rh), _ptr(rb), _ptr(out))
     return out
 
 

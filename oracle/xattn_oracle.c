@@ -115,6 +115,52 @@ void oracle_score_rows(const uint16_t *q, const uint16_t *k, const oracle_dims *
     }
 }
 
+/*
+ * Scoring-pattern variants of the pattern ablation (Sec. 4.5, Table 4): the
+ * S positions summed inside each S x S sub-block are (qsub[t], t), t < S, for
+ * a permutation qsub of 0 .. S-1 (one position per sub-block row and column).
+ * qsub[t] = S-1-t is the antidiagonal of Algorithm 1, qsub[t] = t the main
+ * diagonal, a random permutation the random pattern. Otherwise as
+ * oracle_score_rows: scale 1/(sqrt(d) S), softmax per reduced row over
+ * c <= R (causal), block mass averaged over the block's reduced rows.
+ */
+void oracle_score_pattern_rows(const uint16_t *q, const uint16_t *k, const oracle_dims *d,
+                               int B, int S, const int32_t *qsub, int nrows,
+                               const int32_t *row_h, const int32_t *row_b, double *out)
+{
+    const int L = d->seq, D = d->head_dim, NB = L / B, NR = L / S, nr = B / S;
+    const double scale = 1.0 / (sqrt((double)D) * (double)S);
+#pragma omp parallel for schedule(dynamic, 1)
+    for (int i = 0; i < nrows; ++i) {
+        const int h = row_h[i], b = row_b[i];
+        const uint16_t *Q = q + (size_t)h * L * D;
+        const uint16_t *K = k + (size_t)kv_head(d, h) * L * D;
+        double *row = out + (size_t)i * NB;
+        double *x = (double *)malloc(sizeof(double) * NR);
+        for (int j = 0; j < NB; ++j) row[j] = 0.0;
+        for (int r = 0; r < nr; ++r) {
+            const int R = b * nr + r;
+            const int ncol = d->causal ? R + 1 : NR;
+            for (int c = 0; c < ncol; ++c) {
+                double acc = 0.0;
+                for (int t = 0; t < S; ++t) {
+                    const uint16_t *qr = Q + (size_t)(R * S + qsub[t]) * D;
+                    const uint16_t *kr = K + (size_t)(c * S + t) * D;
+                    for (int e = 0; e < D; ++e) acc += bf(qr[e]) * bf(kr[e]);
+                }
+                x[c] = acc * scale;
+            }
+            double m = -INFINITY;
+            for (int c = 0; c < ncol; ++c) if (x[c] > m) m = x[c];
+            double l = 0.0;
+            for (int c = 0; c < ncol; ++c) l += exp(x[c] - m);
+            for (int c = 0; c < ncol; ++c) row[c / nr] += exp(x[c] - m) / l;
+        }
+        for (int j = 0; j < NB; ++j) row[j] /= (double)nr;
+        free(x);
+    }
+}
+
 typedef struct { uint64_t u; int32_t j; } cand;
 
 static int cand_cmp(const void *a, const void *b)

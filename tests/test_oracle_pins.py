@@ -24,16 +24,20 @@ def f64(u16):
     return W.bf16_bits_to_f32(u16).astype(np.float64)
 
 
-def walk_scores(q, k, B, S, causal, hq_per_kv=1):
+def walk_scores(q, k, B, S, causal, hq_per_kv=1, mask=None):
     """Brute force: full fp64 logits Q K^T, summed over the positions (i, k)
     with (i mod S) + (k mod S) = S - 1 inside each S x S sub-block
     (Sec. 3.2), scaled by 1/(sqrt(d) S), softmaxed per reduced row over the
-    valid reduced columns, block mass averaged over the block's reduced rows."""
+    valid reduced columns, block mass averaged over the block's reduced rows.
+    mask (S x S, bool) replaces the antidiagonal by another sub-block pattern."""
     H, L, D = q.shape
     NB, NR, nr = L // B, L // S, B // S
     out = np.zeros((H, NB, NB))
     ii = np.arange(L)
-    anti = ((ii[:, None] % S) + (ii[None, :] % S)) == S - 1
+    if mask is None:
+        anti = ((ii[:, None] % S) + (ii[None, :] % S)) == S - 1
+    else:
+        anti = np.asarray(mask, bool)[ii[:, None] % S, ii[None, :] % S]
     for h in range(H):
         M = f64(q[h]) @ f64(k[h // hq_per_kv]).T
         Ma = np.where(anti, M, 0.0)
@@ -70,6 +74,30 @@ def test_score_equals_antidiagonal_index_walk(S, causal, D):
     got = oracle.score_rows(q, k, B, S, causal).reshape(2, L // B, L // B)
     want = walk_scores(q, k, B, S, causal, hq_per_kv=2)
     np.testing.assert_allclose(got, want, rtol=1e-10, atol=1e-14)
+
+
+@pytest.mark.parametrize("pattern", ["diagonal", "random", "antidiagonal"])
+@pytest.mark.parametrize("S,causal", [(4, True), (8, False), (8, True)])
+def test_score_pattern_equals_masked_index_walk(pattern, S, causal):
+    # Pattern ablation (Sec. 4.5, Table 4): the S summed positions of each
+    # S x S sub-block form a permutation matrix (one per row and column).
+    # The oracle's pairing qsub must equal the brute-force walk over the full
+    # logits masked by that matrix; the antidiagonal pairing must reproduce
+    # the Algorithm 1 scores exactly.
+    B, L, D = 32, 256, 16
+    q = W.random_bf16((2, L, D), seed=31 + S, scale=1.5)
+    k = W.random_bf16((1, L, D), seed=37 + S, scale=1.5)
+    qsub = {"diagonal": np.arange(S), "antidiagonal": np.arange(S)[::-1],
+            "random": np.random.default_rng(S).permutation(S)}[pattern]
+    mask = np.zeros((S, S), bool)
+    mask[qsub, np.arange(S)] = True
+    assert np.all(mask.sum(0) == 1) and np.all(mask.sum(1) == 1)
+    got = oracle.score_pattern_rows(q, k, B, S, qsub, causal).reshape(2, L // B, L // B)
+    want = walk_scores(q, k, B, S, causal, hq_per_kv=2, mask=mask)
+    np.testing.assert_allclose(got, want, rtol=1e-10, atol=1e-14)
+    if pattern == "antidiagonal":
+        np.testing.assert_array_equal(
+            got, oracle.score_rows(q, k, B, S, causal).reshape(2, L // B, L // B))
 
 
 def test_score_walk_on_clustered_inputs():
