@@ -50,6 +50,11 @@ def parse():
     ap.add_argument("--topk", type=int, default=64, help="key blocks per row (Top-K)")
     ap.add_argument("--ratio", type=float, default=0.05,
                     help="fraction of each row's candidate blocks (Top-Ratio)")
+    ap.add_argument("--pattern", default="antidiagonal",
+                    choices=["antidiagonal", "diagonal", "random"],
+                    help="sampling pattern inside each S x S sub-block of the scoring "
+                         "(random: a permutation drawn from --pattern-seed)")
+    ap.add_argument("--pattern-seed", type=int, default=1)
     ap.add_argument("--dit-schedule", default=None, metavar="T,W",
                     help="video-DiT denoising schedule: time T layer steps (step t uses "
                          "dense attention for t < W, XAttention afterwards); default "
@@ -214,10 +219,19 @@ def main():
         else:
             X.xattn_select_ratio(scores, dims, a.ratio, w.block, idx=idx, cnt=cnt)
 
+    qsub = W.sub_row_pairing(a.pattern, w.stride, seed=a.pattern_seed)
+
+    def score():
+        if a.pattern == "antidiagonal":
+            X.xattn_score(q, k, w.causal, w.block, w.stride, scores=scores, workspace=ws)
+        else:
+            X.xattn_score_pattern(q, k, w.causal, w.block, w.stride, qsub, scores=scores,
+                                  workspace=ws)
+
     def step(ev=None):
         if ev is not None:
             ev[0].record(stream)
-        X.xattn_score(q, k, w.causal, w.block, w.stride, scores=scores, workspace=ws)
+        score()
         if ev is not None:
             ev[1].record(stream)
         select()
@@ -313,7 +327,9 @@ def main():
         "vs_baseline": None,
         "dtype": "bf16",
         "data": "synthetic",
-        "config": dict(w.describe(), **({} if a.select_mode == "threshold" else {
+        "config": dict(w.describe(), **({} if a.pattern == "antidiagonal" else {
+            "pattern": {"name": a.pattern, "qsub": qsub.tolist()}}), **({}
+            if a.select_mode == "threshold" else {
             "select": {"heads": {"tau_h": [round(float(t), 4) for t in tau_h]},
                        "topk": {"k_blocks": a.topk},
                        "ratio": {"ratio": a.ratio}}[a.select_mode] | {"mode": a.select_mode}})),

@@ -83,6 +83,23 @@ int xattn_score(const void *q, const void *k, const xattn_dims *dims, int block,
                 void *stream);
 
 /*
+ * Step 1 with another sampling pattern inside each S x S sub-block (the
+ * pattern ablation, Sec. 4.5, Table 4): the S summed positions are
+ * (query sub-row qsub[t], key sub-row t), t < S, so
+ *   X[R][c] = (1 / (S sqrt(D))) sum_{t<S} q[R*S + qsub[t]] . k[c*S + t].
+ * qsub[t] = S-1-t is xattn_score (the antidiagonal); qsub[t] = t the main
+ * diagonal; any other permutation (e.g. a seeded random one) the random
+ * pattern, which keeps one position per sub-block row and column.
+ *   qsub  host array of `stride` int32, a permutation of 0 .. stride-1; read
+ *         during the call only (copied into the launch)
+ * Everything else as xattn_score. XATTN_ERR_ARG if qsub is NULL or not a
+ * permutation.
+ */
+int xattn_score_pattern(const void *q, const void *k, const xattn_dims *dims, int block,
+                        int stride, const int32_t *qsub, float *scores, void *workspace,
+                        size_t workspace_bytes, void *stream);
+
+/*
  * Step 2 -- threshold block selection, find_blocks (Sec. 3.2, equation of
  * find_blocks; Algorithm 1). Per row (h, b) the candidates are j <= b
  * (causal) or all j. Each candidate's mass is taken as the integer

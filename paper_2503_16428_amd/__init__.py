@@ -5,6 +5,7 @@ in-tree build (build.py) and a thin ctypes binding (binding.py)."""
 from .binding import (  # noqa: F401
     BLOCK, Dims, XAttnError, forward_layout, forward_workspace_size, lib, lib_path,
     make_dims, score_workspace_size, version, xattn_block_sparse_attn, xattn_dense_attn,
-    xattn_forward, xattn_forward_scheduled, xattn_score, xattn_select, xattn_select_heads,
+    xattn_forward, xattn_forward_scheduled, xattn_score,
+    xattn_score_pattern, xattn_select, xattn_select_heads,
     xattn_select_ratio, xattn_select_topk,
 )

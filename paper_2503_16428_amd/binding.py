@@ -56,7 +56,8 @@ class Dims(ctypes.Structure):
 
 
 EXPORTS = [
-    "xattn_score_workspace_size", "xattn_score", "xattn_select", "xattn_select_heads",
+    "xattn_score_workspace_size", "xattn_score", "xattn_score_pattern", "xattn_select",
+    "xattn_select_heads",
     "xattn_select_topk", "xattn_select_ratio", "xattn_block_sparse_attn",
     "xattn_dense_attn", "xattn_forward_workspace_size", "xattn_forward_layout",
     "xattn_forward", "xattn_forward_scheduled", "xattn_strerror", "xattn_last_error",
@@ -80,6 +81,7 @@ def lib() -> ctypes.CDLL:
         PSZ = ctypes.POINTER(SZ)
         L.xattn_score_workspace_size.argtypes = [PD, I, I, PSZ]
         L.xattn_score.argtypes = [P, P, PD, I, I, P, P, SZ, P]
+        L.xattn_score_pattern.argtypes = [P, P, PD, I, I, P, P, P, SZ, P]
         L.xattn_select.argtypes = [P, PD, I, F, P, P, P]
         L.xattn_select_heads.argtypes = [P, PD, I, P, P, P, P]
         L.xattn_select_topk.argtypes = [P, PD, I, P, P, P, P]
@@ -173,6 +175,26 @@ def xattn_score(q, k, causal=True, block=BLOCK, stride=8, scores=None, workspace
                                 device=q.device)
     _check(lib().xattn_score(_ptr(q), _ptr(k), ctypes.byref(d), block, stride, _ptr(scores),
                              _ptr(workspace), workspace.numel(), _stream(stream)))
+    return scores
+
+
+def xattn_score_pattern(q, k, causal, block, stride, qsub, scores=None, workspace=None,
+                        stream=None):
+    """Block scores with the sub-block positions (qsub[t], t): qsub a permutation of
+    0..stride-1 (stride-1-t is the antidiagonal of xattn_score, t the diagonal)."""
+    _need(q, torch.bfloat16, "q")
+    _need(k, torch.bfloat16, "k")
+    d = make_dims(q, k, causal)
+    nb = d.seq // block
+    if scores is None:
+        scores = torch.empty((d.heads, nb, nb), dtype=torch.float32, device=q.device)
+    if workspace is None:
+        workspace = torch.empty(score_workspace_size(d, block, stride), dtype=torch.uint8,
+                                device=q.device)
+    qs = np.ascontiguousarray(qsub, dtype=np.int32)
+    _check(lib().xattn_score_pattern(_ptr(q), _ptr(k), ctypes.byref(d), block, stride,
+                                     qs.ctypes.data_as(ctypes.c_void_p), _ptr(scores),
+                                     _ptr(workspace), workspace.numel(), _stream(stream)))
     return scores
 
 

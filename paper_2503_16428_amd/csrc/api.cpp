@@ -133,8 +133,33 @@ int xattn_score(const void* q, const void* k, const xattn_dims* dims, int block,
   if (!workspace || workspace_bytes < need)
     return fail(XATTN_ERR_WORKSPACE, "workspace of %zu bytes needed, %zu given", need,
                 workspace ? workspace_bytes : (size_t)0);
-  return hip_status(launch_score(q, k, s, stride, scores, workspace, (hipStream_t)stream),
+  return hip_status(launch_score(q, k, s, stride, nullptr, scores, workspace,
+                                  (hipStream_t)stream),
                     "xattn_score launch");
+}
+
+int xattn_score_pattern(const void* q, const void* k, const xattn_dims* dims, int block,
+                        int stride, const int32_t* qsub, float* scores, void* workspace,
+                        size_t workspace_bytes, void* stream) {
+  XattnShape s;
+  int rc;
+  if ((rc = check_dims(dims, &s)) || (rc = check_block(block)) || (rc = check_stride(stride)))
+    return rc;
+  if (!qsub) return fail(XATTN_ERR_ARG, "qsub is NULL");
+  bool seen[64] = {};
+  for (int t = 0; t < stride; ++t) {
+    if (qsub[t] < 0 || qsub[t] >= stride || seen[qsub[t]])
+      return fail(XATTN_ERR_ARG, "qsub must be a permutation of 0..%d (qsub[%d] = %d)",
+                  stride - 1, t, qsub[t]);
+    seen[qsub[t]] = true;
+  }
+  if (!q || !k || !scores) return fail(XATTN_ERR_ARG, "q, k and scores must be non-NULL");
+  const size_t need = score_scratch_bytes(s, stride);
+  if (!workspace || workspace_bytes < need)
+    return fail(XATTN_ERR_WORKSPACE, "workspace of %zu bytes needed, %zu given", need,
+                workspace ? workspace_bytes : (size_t)0);
+  return hip_status(launch_score(q, k, s, stride, qsub, scores, workspace, (hipStream_t)stream),
+                    "xattn_score_pattern launch");
 }
 
 int xattn_select(const float* scores, const xattn_dims* dims, int block, float tau,
@@ -270,7 +295,7 @@ int xattn_forward(const void* q, const void* k, const void* v, const xattn_dims*
   int32_t* idx = (int32_t*)(ws + o_idx);
   int32_t* cnt = (int32_t*)(ws + o_cnt);
   hipStream_t st = (hipStream_t)stream;
-  hipError_t e = launch_score(q, k, s, stride, sc, ws + o_scr, st);
+  hipError_t e = launch_score(q, k, s, stride, nullptr, sc, ws + o_scr, st);
   if (e == hipSuccess) e = launch_select(sc, s, uniform_threshold(s, tau), idx, cnt, st);
   if (e == hipSuccess) e = launch_attn(q, k, v, s, idx, cnt, false, o, lse, st);
   return hip_status(e, "xattn_forward launch");

@@ -88,8 +88,14 @@ struct XattnShape {
   int NB() const { return seq / xattn::kBlock; }
 };
 
+// Query sub-row paired with key sub-row t inside each S x S sub-block of the
+// scoring: S-1-t is the antidiagonal of Algorithm 1 (qsub == nullptr); other
+// permutations give the diagonal / random patterns. Passed by value.
+struct SubRowPairing {
+  int q[64];
+};
 hipError_t launch_score(const void* q, const void* k, const XattnShape& s, int stride,
-                        float* scores, void* scratch, hipStream_t st);
+                        const int32_t* qsub, float* scores, void* scratch, hipStream_t st);
 size_t score_scratch_bytes(const XattnShape& s, int stride);
 // Selection rule of one launch: find_blocks with a threshold per head, or a
 // fixed block count per head (Top-K) or fraction of the candidates

@@ -60,7 +60,7 @@ template <int NRB, bool CAUSAL>
 __global__ __launch_bounds__(kThreads, 1) void score_partials(
     const uint16_t* __restrict__ q, const uint16_t* __restrict__ k, int hq, int hkv, int L,
     int NR, int NB, int NT, int tiles_per_head, int n_work, float scale_log2,
-    float* __restrict__ part, float2* __restrict__ stats) {
+    SubRowPairing pairing, float* __restrict__ part, float2* __restrict__ stats) {
   constexpr int S = kBlock / NRB;
   constexpr int KD = S * kHeadDim;  // reduced inner dimension S*d
   constexpr int NCH = KD / KC;      // >= 2 (S >= 1)
@@ -108,7 +108,7 @@ __global__ __launch_bounds__(kThreads, 1) void score_partials(
     const int tsub = kap0 / kHeadDim, e0 = kap0 % kHeadDim;
     const uint32_t st = lds0 + (uint32_t)((ch % NSTAGE) * 2 * kStage * 2);
     const uint16_t* baseA = Kg + kap0;
-    const uint16_t* baseB = Qh + (S - 1 - tsub) * kHeadDim + e0;
+    const uint16_t* baseB = Qh + pairing.q[tsub] * kHeadDim + e0;
 #pragma unroll
     for (int i = 0; i < kDmaPerOp; ++i) {
       const uint32_t row_lds = (uint32_t)((32 * wv + kDmaRows * i) * KC * 2);
@@ -411,8 +411,8 @@ __global__ __launch_bounds__(256) void score_finalize(const float* __restrict__ 
 }
 
 template <int NRB, bool CAUSAL>
-hipError_t launch_partials(const void* q, const void* k, const XattnShape& s, float* part,
-                           float* stats, hipStream_t st) {
+hipError_t launch_partials(const void* q, const void* k, const XattnShape& s,
+                           const SubRowPairing& pr, float* part, float* stats, hipStream_t st) {
   const int S = kBlock / NRB, NR = s.seq / S, NB = s.NB(), NT = ceil_div(NR, TSUB);
   const int T = ceil_div(NR, TM);
   const int tiles = CAUSAL ? T * (T + 1) / 2 : T * T;
@@ -420,15 +420,15 @@ hipError_t launch_partials(const void* q, const void* k, const XattnShape& s, fl
   const float scale_log2 = kLog2e / (sqrtf((float)kHeadDim) * (float)S);
   hipLaunchKernelGGL((score_partials<NRB, CAUSAL>), dim3(n_work), dim3(kThreads), 0, st,
                      (const uint16_t*)q, (const uint16_t*)k, s.hq, s.hkv, s.seq, NR, NB, NT,
-                     tiles, n_work, scale_log2, part, (float2*)stats);
+                     tiles, n_work, scale_log2, pr, part, (float2*)stats);
   return hipGetLastError();
 }
 
 template <int NRB>
-hipError_t launch_partials_c(const void* q, const void* k, const XattnShape& s, float* part,
-                             float* stats, hipStream_t st) {
-  return s.causal ? launch_partials<NRB, true>(q, k, s, part, stats, st)
-                  : launch_partials<NRB, false>(q, k, s, part, stats, st);
+hipError_t launch_partials_c(const void* q, const void* k, const XattnShape& s,
+                             const SubRowPairing& pr, float* part, float* stats, hipStream_t st) {
+  return s.causal ? launch_partials<NRB, true>(q, k, s, pr, part, stats, st)
+                  : launch_partials<NRB, false>(q, k, s, pr, part, stats, st);
 }
 
 }  // namespace
@@ -441,20 +441,22 @@ size_t score_scratch_bytes(const XattnShape& s, int stride) {
 }
 
 hipError_t launch_score(const void* q, const void* k, const XattnShape& s, int stride,
-                        float* scores, void* scratch, hipStream_t st) {
+                        const int32_t* qsub, float* scores, void* scratch, hipStream_t st) {
+  SubRowPairing pr;
+  for (int t = 0; t < stride; ++t) pr.q[t] = qsub ? qsub[t] : stride - 1 - t;
   const int NR = s.seq / stride, NB = s.NB(), NT = ceil_div(NR, TSUB);
   const size_t part_bytes = (size_t)s.HQ() * NR * NB * sizeof(float);
   float* part = (float*)scratch;
   float* stats = (float*)((char*)scratch + ((part_bytes + 255) / 256) * 256);
   hipError_t e;
   switch (stride) {
-    case 1: e = launch_partials_c<128>(q, k, s, part, stats, st); break;
-    case 2: e = launch_partials_c<64>(q, k, s, part, stats, st); break;
-    case 4: e = launch_partials_c<32>(q, k, s, part, stats, st); break;
-    case 8: e = launch_partials_c<16>(q, k, s, part, stats, st); break;
-    case 16: e = launch_partials_c<8>(q, k, s, part, stats, st); break;
-    case 32: e = launch_partials_c<4>(q, k, s, part, stats, st); break;
-    case 64: e = launch_partials_c<2>(q, k, s, part, stats, st); break;
+    case 1: e = launch_partials_c<128>(q, k, s, pr, part, stats, st); break;
+    case 2: e = launch_partials_c<64>(q, k, s, pr, part, stats, st); break;
+    case 4: e = launch_partials_c<32>(q, k, s, pr, part, stats, st); break;
+    case 8: e = launch_partials_c<16>(q, k, s, pr, part, stats, st); break;
+    case 16: e = launch_partials_c<8>(q, k, s, pr, part, stats, st); break;
+    case 32: e = launch_partials_c<4>(q, k, s, pr, part, stats, st); break;
+    case 64: e = launch_partials_c<2>(q, k, s, pr, part, stats, st); break;
     default: return hipErrorInvalidValue;
   }
   if (e != hipSuccess) return e;

@@ -29,21 +29,23 @@ def host_f32(t) -> np.ndarray:
     return t.float().cpu().numpy()
 
 
-def logit_error_bound(q, k, S, rows_h, rows_b, hq_per_kv, B=128):
+def logit_error_bound(q, k, S, rows_h, rows_b, hq_per_kv, B=128, qsub=None):
     """Rigorous bound on |z_gpu - z_exact| for the reduced logits of the given
     rows: the GPU sums n = S*d exact bf16 products in fp32 (any order), so
     |error| <= gamma_n * sum |q_e k_e| with gamma_n = n u / (1 - n u), then
-    scales by 1/(S sqrt d) (one more rounding)."""
+    scales by 1/(S sqrt d) (one more rounding). qsub: the sub-row pairing
+    (default the antidiagonal, S-1-t)."""
     D = q.shape[-1]
     n = S * D
     gamma = n * U32 / (1 - n * U32)
     worst = 0.0
     nr = B // S
+    pair = np.arange(S)[::-1] if qsub is None else np.asarray(qsub)
     for h, b in zip(rows_h, rows_b):
         qa = np.abs(W.bf16_bits_to_f32(q[h]))
         ka = np.abs(W.bf16_bits_to_f32(k[h // hq_per_kv]))
         R0 = b * nr
-        Qr = np.stack([qa[(R0 + r) * S:(R0 + r + 1) * S][::-1].reshape(-1) for r in range(nr)])
+        Qr = np.stack([qa[(R0 + r) * S + pair].reshape(-1) for r in range(nr)])
         Kt = ka.reshape(-1, n)
         worst = max(worst, float((Qr @ Kt.T).max()))
     return (gamma * worst + U32 * 4 * worst / n) / (S * math.sqrt(D))

@@ -160,3 +160,18 @@ def test_scheduled_forward_validates_before_launch():
     # a sparse step needs the workspace
     assert L.xattn_forward_scheduled(fake, fake, fake, ctypes.byref(d), 128, 8, 0.9, 5, 5,
                                      fake, None, None, 0, None) == B.XATTN_ERR_WORKSPACE
+
+
+def test_pattern_scoring_validates_before_launch():
+    L = X.lib()
+    d = _dims()
+    fake = ctypes.c_void_p(0x1000)   # never dereferenced: every case fails validation
+    for bad in ([0, 1, 2, 3, 4, 5, 6, 6], [0, 1, 2, 3, 4, 5, 6, 8], [-1, 1, 2, 3, 4, 5, 6, 7]):
+        a = (ctypes.c_int32 * 8)(*bad)
+        assert L.xattn_score_pattern(fake, fake, ctypes.byref(d), 128, 8, a, fake, fake,
+                                     1 << 40, None) == B.XATTN_ERR_ARG
+    assert L.xattn_score_pattern(fake, fake, ctypes.byref(d), 128, 8, None, fake, fake,
+                                 1 << 40, None) == B.XATTN_ERR_ARG
+    a = (ctypes.c_int32 * 8)(*range(8))
+    assert L.xattn_score_pattern(fake, fake, ctypes.byref(d), 128, 8, a, fake, None, 0,
+                                 None) == B.XATTN_ERR_WORKSPACE

@@ -230,3 +230,16 @@ def random_score_rows(n_rows: int, n_blocks: int, seed: int, causal: bool = True
             x = rng.gamma(0.3, 1.0, m)
         s[r, :m] = x / x.sum()
     return s.astype(np.float32), b.astype(np.int32)
+
+
+def sub_row_pairing(pattern: str, stride: int, seed: int = 0) -> np.ndarray:
+    """Sampling pattern inside each S x S sub-block as the query sub-row paired
+    with key sub-row t: 'antidiagonal' (S-1-t), 'diagonal' (t) or 'random' (a
+    permutation drawn from seed), int32."""
+    if pattern == "antidiagonal":
+        return np.arange(stride - 1, -1, -1, dtype=np.int32)
+    if pattern == "diagonal":
+        return np.arange(stride, dtype=np.int32)
+    if pattern == "random":
+        return np.random.default_rng(seed).permutation(stride).astype(np.int32)
+    raise ValueError(f"unknown pattern {pattern!r}")
