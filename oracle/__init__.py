@@ -16,6 +16,13 @@ and library routines, never against the oracle itself):
   sparse/dense    -- textbook masked softmax attention (torch fp64 CPU SDPA and
                      numpy), zero-query closed form.
   block_mass_rows -- (diagnostic) numpy softmax block sums.
+  select_topk/ratio_rows -- upper set of the find_blocks order, brute-force
+                     maximal mass, equality with find_blocks at its count,
+                     hand-derived ratio counts.
+  score_pattern_rows -- brute-force walk over the logits masked by the
+                     sub-block permutation; antidiagonal == score_rows.
+  threshold_dp    -- (thresholds.py) enumeration of every adjustment
+                     assignment, top-M gains for one adjustment per head.
 
 Array conventions: bf16 tensors are uint16 bit patterns [heads][seq][d];
 a "row" is one (query head, query block) pair.
@@ -219,3 +226,8 @@ def forward_rows(q, k, v, B, S, tau, causal=True, rows=None, batch=1):
     idx, cnt = select_rows(sc, rb, tau, causal)
     o, lse = sparse_attn_rows(q, k, v, B, idx, cnt, causal, (rh, rb), batch)
     return {"scores": sc, "idx": idx, "cnt": cnt, "o": o, "lse": lse}
+
+
+from .thresholds import (  # noqa: E402,F401
+    head_errors, threshold_dp, thresholds_from_adjustments,
+)
