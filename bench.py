@@ -55,6 +55,10 @@ def parse():
                     help="sampling pattern inside each S x S sub-block of the scoring "
                          "(random: a permutation drawn from --pattern-seed)")
     ap.add_argument("--pattern-seed", type=int, default=1)
+    ap.add_argument("--predict-thresholds", default=None, metavar="M[,A]",
+                    help="before timing, predict per-head thresholds (Sec. 3.3): M 10 %% "
+                         "reductions from tau over the query heads, at most A per head "
+                         "(default 1); the step then selects with those thresholds")
     ap.add_argument("--dit-schedule", default=None, metavar="T,W",
                     help="video-DiT denoising schedule: time T layer steps (step t uses "
                          "dense attention for t < W, XAttention afterwards); default "
@@ -208,6 +212,25 @@ def main():
         return
     lo_hi = [float(t) for t in a.tau_heads.split(",")]
     tau_h = np.linspace(lo_hi[0], lo_hi[-1], w.hq).astype(np.float32)
+    prediction = None
+    if a.predict_thresholds:
+        parts = [int(t) for t in a.predict_thresholds.split(",")]
+        M, A = parts[0], (parts[1] if len(parts) > 1 else 1)
+        t0 = time.perf_counter()
+        res = X.predict_thresholds(q, k, v, M, tau0=w.tau, max_adjust=A, causal=w.causal,
+                                   block=w.block, stride=w.stride)
+        torch.cuda.synchronize()
+        tau_h = res["tau_h"]
+        a.select_mode = "heads"
+        err = res["err"]
+        prediction = {
+            "adjustments": M, "max_per_head": A, "seconds": round(time.perf_counter() - t0, 3),
+            "mean_tau": round(float(tau_h.mean()), 4),
+            "mean_head_error_uniform_tau": round(float(err[:, 0].mean()), 6),
+            "mean_head_error_predicted": round(float(np.mean(
+                [err[h, j] for h, j in enumerate(res["adjust"])])), 6),
+        }
+        print(f"# predicted thresholds {tau_h.round(4).tolist()}", file=sys.stderr, flush=True)
 
     def select():
         if a.select_mode == "threshold":
@@ -348,6 +371,8 @@ def main():
         "roofline": roofline,
         "cpu_baseline": cpu,
     }
+    if prediction is not None:
+        out["threshold_prediction"] = prediction
     print(json.dumps(out), flush=True)
 
 

@@ -208,6 +208,38 @@ int xattn_forward_scheduled(const void *q, const void *k, const void *v,
                             int step, int warmup_steps, void *o, float *lse,
                             void *workspace, size_t workspace_bytes, void *stream);
 
+/*
+ * Minimum-threshold prediction (Sec. 3.3). The paper fills a table D[h][m],
+ * the best performance reachable with exactly m threshold adjustments over
+ * the first h heads, each adjustment lowering one head's threshold by 10 %
+ * (t <- 0.9 t); head h either keeps D[h-1][m] or takes one more adjustment on
+ * top of D[h-1][m-1]. Here a head may take up to max_adjust adjustments
+ * (max_adjust = 1 is the paper's recurrence) and performance is additive over
+ * heads, given as a table from the caller (for instance minus each head's
+ * output error at each adjusted threshold, from xattn_head_error).
+ *   perf         host double [heads][max_adjust + 1]: perf[h][a] is head h's
+ *                performance after a adjustments; finite
+ *   adjustments  M, the total number of adjustments, 0 <= M <= heads * max_adjust
+ *   adjust       host int32 [heads] (output): adjustments per head, summing
+ *                to M; the threshold of head h becomes t0 * 0.9^adjust[h]
+ *   best         host double (output, may be NULL): D[heads][M]
+ * On equal performance a head keeps fewer adjustments. Host only (no GPU).
+ */
+int xattn_threshold_dp(const double *perf, int heads, int max_adjust, int adjustments,
+                       int32_t *adjust, double *best);
+
+/*
+ * Per-head output error, the performance proxy for xattn_threshold_dp:
+ * err[h] = sum (o - o_ref)^2 / sum o_ref^2 over head h's [L][D] outputs
+ * (bf16 inputs, fp64 accumulation, a fixed order: deterministic).
+ *   o, o_ref   bf16 [HQ][L][D] device
+ *   err        double [HQ] device (output)
+ *   workspace  at least xattn_head_error_workspace_size() bytes of device memory
+ */
+int xattn_head_error_workspace_size(const xattn_dims *dims, size_t *bytes);
+int xattn_head_error(const void *o, const void *o_ref, const xattn_dims *dims, double *err,
+                     void *workspace, size_t workspace_bytes, void *stream);
+
 /* Static description of a status code (never NULL). */
 const char *xattn_strerror(int status);
 /* Message describing the last failure on the calling thread ("" if none). */

@@ -60,7 +60,8 @@ EXPORTS = [
     "xattn_select_heads",
     "xattn_select_topk", "xattn_select_ratio", "xattn_block_sparse_attn",
     "xattn_dense_attn", "xattn_forward_workspace_size", "xattn_forward_layout",
-    "xattn_forward", "xattn_forward_scheduled", "xattn_strerror", "xattn_last_error",
+    "xattn_forward", "xattn_forward_scheduled", "xattn_threshold_dp",
+    "xattn_head_error_workspace_size", "xattn_head_error", "xattn_strerror", "xattn_last_error",
     "xattn_version",
 ]
 
@@ -92,6 +93,9 @@ def lib() -> ctypes.CDLL:
         L.xattn_forward_layout.argtypes = [PD, I, I, PSZ, PSZ, PSZ, PSZ]
         L.xattn_forward.argtypes = [P, P, P, PD, I, I, F, P, P, P, SZ, P]
         L.xattn_forward_scheduled.argtypes = [P, P, P, PD, I, I, F, I, I, P, P, P, SZ, P]
+        L.xattn_threshold_dp.argtypes = [P, I, I, I, P, P]
+        L.xattn_head_error_workspace_size.argtypes = [PD, PSZ]
+        L.xattn_head_error.argtypes = [P, P, PD, P, P, SZ, P]
         L.xattn_strerror.argtypes = [I]
         L.xattn_strerror.restype = ctypes.c_char_p
         L.xattn_last_error.restype = ctypes.c_char_p
@@ -342,6 +346,37 @@ def xattn_forward_scheduled(q, k, v, step, warmup_steps=5, causal=False, block=B
                                          0 if workspace is None else workspace.numel(),
                                          _stream(stream)))
     return o, lse
+
+
+def threshold_dp(perf, adjustments: int):
+    """Minimum-threshold dynamic program over a per-head performance table
+    perf [heads][max_adjust + 1] (host). Returns (adjust int32 [heads], best)."""
+    p = np.ascontiguousarray(perf, dtype=np.float64)
+    if p.ndim != 2 or p.shape[1] < 2:
+        raise XAttnError(XATTN_ERR_ARG, f"perf must be [heads][max_adjust + 1], got {p.shape}")
+    adj = np.zeros(p.shape[0], dtype=np.int32)
+    best = ctypes.c_double(0.0)
+    _check(lib().xattn_threshold_dp(p.ctypes.data_as(ctypes.c_void_p), p.shape[0],
+                                    p.shape[1] - 1, int(adjustments),
+                                    adj.ctypes.data_as(ctypes.c_void_p), ctypes.byref(best)))
+    return adj, best.value
+
+
+def head_error(o, o_ref, causal=True, workspace=None, stream=None):
+    """Per-head relative squared error of o against o_ref (float64 [heads] on the device)."""
+    _need(o, torch.bfloat16, "o")
+    _need(o_ref, torch.bfloat16, "o_ref")
+    if o.shape != o_ref.shape:
+        raise XAttnError(XATTN_ERR_ARG, "o and o_ref must have the same shape")
+    d = make_dims(o, o if o.dim() == 3 else o, causal)
+    n = ctypes.c_size_t(0)
+    _check(lib().xattn_head_error_workspace_size(ctypes.byref(d), ctypes.byref(n)))
+    if workspace is None:
+        workspace = torch.empty(max(n.value, 1), dtype=torch.uint8, device=o.device)
+    err = torch.empty(d.heads, dtype=torch.float64, device=o.device)
+    _check(lib().xattn_head_error(_ptr(o), _ptr(o_ref), ctypes.byref(d), _ptr(err),
+                                  _ptr(workspace), workspace.numel(), _stream(stream)))
+    return err
 
 
 def version() -> int:

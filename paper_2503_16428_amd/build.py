@@ -15,7 +15,7 @@ ROOT = os.path.dirname(HERE)
 CSRC = os.path.join(HERE, "csrc")
 OUT_DIR = os.path.join(HERE, "lib")
 LIB = os.path.join(OUT_DIR, "libxattn.so")
-SOURCES = ["score.hip", "select.hip", "attn.hip", "api.cpp"]
+SOURCES = ["score.hip", "select.hip", "attn.hip", "error.hip", "api.cpp", "threshold.cpp"]
 ARCH = "gfx950"
 
 COMMON_FLAGS = [

@@ -11,10 +11,11 @@
 #include "xattn.h"
 #include "common.h"
 
-namespace {
+namespace xattn_host {
 
 thread_local char g_err[512] = "";
 
+// Records the message of a failing call (read back by xattn_last_error).
 int fail(int code, const char* fmt, ...) {
   va_list ap;
   va_start(ap, fmt);
@@ -22,6 +23,13 @@ int fail(int code, const char* fmt, ...) {
   va_end(ap);
   return code;
 }
+
+}  // namespace xattn_host
+
+namespace {
+
+using xattn_host::fail;
+using xattn_host::g_err;
 
 int ok() {
   g_err[0] = '\0';
@@ -318,6 +326,30 @@ int xattn_forward_scheduled(const void* q, const void* k, const void* v, const x
   }
   return xattn_forward(q, k, v, dims, block, stride, tau, o, lse, workspace, workspace_bytes,
                        stream);
+}
+
+int xattn_head_error_workspace_size(const xattn_dims* dims, size_t* bytes) {
+  XattnShape s;
+  int rc;
+  if ((rc = check_dims(dims, &s))) return rc;
+  if (!bytes) return fail(XATTN_ERR_ARG, "bytes is NULL");
+  *bytes = head_error_scratch_bytes(s);
+  return ok();
+}
+
+int xattn_head_error(const void* o, const void* o_ref, const xattn_dims* dims, double* err,
+                     void* workspace, size_t workspace_bytes, void* stream) {
+  XattnShape s;
+  int rc;
+  if ((rc = check_dims(dims, &s))) return rc;
+  if (s.HQ() > 65535) return fail(XATTN_ERR_UNSUPPORTED, "more than 65535 heads");
+  if (!o || !o_ref || !err) return fail(XATTN_ERR_ARG, "o, o_ref and err must be non-NULL");
+  const size_t need = head_error_scratch_bytes(s);
+  if (!workspace || workspace_bytes < need)
+    return fail(XATTN_ERR_WORKSPACE, "workspace of %zu bytes needed, %zu given", need,
+                workspace ? workspace_bytes : (size_t)0);
+  return hip_status(launch_head_error(o, o_ref, s, err, workspace, (hipStream_t)stream),
+                    "xattn_head_error launch");
 }
 
 const char* xattn_strerror(int status) {
