@@ -193,19 +193,30 @@ __global__ __launch_bounds__(kThreads, 1) void score_partials(
 #pragma unroll
   for (int n = 0; n < 2; ++n) {
     const int R = R0 + 64 * wr + 32 * n + lr;
+    // Invalid columns (c > R when causal, c >= NR) occur only in sub-tiles
+    // that reach past the slab's first row or the reduced length; the empty
+    // asm keeps this uniform branch from becoming selects on every tile.
+    const int Rslab = R0 + 64 * wr + 32 * n;
+    if ((CAUSAL && csub + 127 > Rslab) || csub + 127 >= NR) {
+      asm volatile("");
+#pragma unroll
+      for (int t = 0; t < 4; ++t) {
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          const int c = csub + 32 * t + 8 * (r >> 2) + 4 * lh + (r & 3);
+          if (c >= NR || (CAUSAL && c > R)) acc[t][n][r] = -INFINITY;
+        }
+      }
+    }
+    // max of the raw products (the scale is positive), then every term as
+    // one fma inside the exponential: p = 2^(x scale - m)
     float mloc = -INFINITY;
 #pragma unroll
     for (int t = 0; t < 4; ++t) {
 #pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const int c = csub + 32 * t + 8 * (r >> 2) + 4 * lh + (r & 3);
-        const bool valid = (c < NR) && (!CAUSAL || c <= R);
-        const float x = valid ? acc[t][n][r] * scale_log2 : -INFINITY;
-        acc[t][n][r] = x;
-        mloc = fmaxf(mloc, x);
-      }
+      for (int r = 0; r < 16; ++r) mloc = fmaxf(mloc, acc[t][n][r]);
     }
-    const float m = fmaxf(mloc, __shfl_xor(mloc, 32));
+    const float m = fmaxf(mloc, __shfl_xor(mloc, 32)) * scale_log2;
     const float mref = (m == -INFINITY) ? 0.f : m;
     float gsum[16];  // groups of 4 consecutive columns: group gi = 4 t + r / 4
     float lloc = 0.f;
@@ -216,7 +227,7 @@ __global__ __launch_bounds__(kThreads, 1) void score_partials(
         float sum = 0.f;
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
-          const float p = fast_exp2(acc[t][n][4 * g4 + e] - mref);
+          const float p = fast_exp2(fmaf(acc[t][n][4 * g4 + e], scale_log2, -mref));
           acc[t][n][4 * g4 + e] = p;
           sum += p;
         }
