@@ -59,6 +59,10 @@ def parse():
                     help="before timing, predict per-head thresholds (Sec. 3.3): M 10 %% "
                          "reductions from tau over the query heads, at most A per head "
                          "(default 1); the step then selects with those thresholds")
+    ap.add_argument("--sweep", action="store_true",
+                    help="the 64K parameter sweep: tau in {0.8, 0.9, 0.95} x S in {4, 8, 16} "
+                         "plus tau = 1 (S = 8); per point the layer time, stage times and "
+                         "density; one JSON line with every point")
     ap.add_argument("--dit-schedule", default=None, metavar="T,W",
                     help="video-DiT denoising schedule: time T layer steps (step t uses "
                          "dense attention for t < W, XAttention afterwards); default "
@@ -128,6 +132,69 @@ def read_traffic(path, w, kernel):
     return None
 
 
+def sweep_main(a, w, q, k, v, dims, stream):
+    """Every (tau, S) point of the sweep on the same inputs: K timed steps of
+    score -> select -> sparse attention each, HIP events per stage."""
+    import torch
+    import paper_2503_16428_amd as X
+    NB = w.n_blocks
+    scores = torch.empty((dims.heads, NB, NB), dtype=torch.float32, device=q.device)
+    idx = torch.empty((dims.heads, NB, NB), dtype=torch.int32, device=q.device)
+    cnt = torch.empty((dims.heads, NB), dtype=torch.int32, device=q.device)
+    o = torch.empty_like(q)
+    points = []
+    dflops = dense_flops(w)
+    for tau, S in W.C4_SWEEP:
+        ws = torch.empty(X.score_workspace_size(dims, w.block, S), dtype=torch.uint8,
+                         device=q.device)
+
+        def step(ev=None):
+            if ev is not None:
+                ev[0].record(stream)
+            X.xattn_score(q, k, w.causal, w.block, S, scores=scores, workspace=ws)
+            if ev is not None:
+                ev[1].record(stream)
+            X.xattn_select(scores, dims, tau, w.block, idx=idx, cnt=cnt)
+            if ev is not None:
+                ev[2].record(stream)
+            X.xattn_block_sparse_attn(q, k, v, idx, cnt, w.causal, w.block, o=o,
+                                      want_lse=False)
+            if ev is not None:
+                ev[3].record(stream)
+
+        for _ in range(a.warmup):
+            step()
+        torch.cuda.synchronize()
+        evs = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(a.steps)]
+        t0 = time.perf_counter()
+        for i in range(a.steps):
+            step(evs[i])
+        torch.cuda.synchronize()
+        ms = (time.perf_counter() - t0) * 1e3 / a.steps
+        st = np.array([[e[0].elapsed_time(e[1]), e[1].elapsed_time(e[2]),
+                        e[2].elapsed_time(e[3])] for e in evs]).mean(0)
+        c = cnt.cpu().numpy().astype(np.int64)
+        dens = float(c.sum() / ((np.arange(1, NB + 1) if w.causal else np.full(NB, NB)).sum()
+                               * dims.heads))
+        points.append({"tau": tau, "stride": S, "ms_per_step": round(ms, 4),
+                       "stages_ms": {"score": round(float(st[0]), 4),
+                                     "select": round(float(st[1]), 4),
+                                     "attn": round(float(st[2]), 4)},
+                       "density": round(dens, 5),
+                       "dense_equiv_tflops": round(dflops / (ms * 1e-3) / 1e12, 1)})
+        print(f"# tau={tau} S={S}: {ms:.3f} ms, density {dens:.4f}", file=sys.stderr, flush=True)
+    ref = next(p for p in points if p["tau"] == 0.9 and p["stride"] == w.stride)
+    out = {
+        "metric": "ms/layer + dense-equiv TFLOP/s of scored block-sparse prefill, 64K sweep",
+        "value": ref["dense_equiv_tflops"], "unit": "TFLOP/s (dense-equivalent)",
+        "n_gpus": 1, "steps": a.steps, "warmup": a.warmup, "ms_per_step": ref["ms_per_step"],
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "bf16",
+        "data": "synthetic", "config": dict(w.describe(), sweep="tau x S; value at tau=0.9, S=8"),
+        "sweep": points, "roofline": None, "cpu_baseline": None,
+    }
+    print(json.dumps(out), flush=True)
+
+
 def schedule_main(a, w, q, k, v, dims, stream):
     """One video-DiT denoising run per T steps: layer step t runs dense
     attention for t < W and score -> select -> sparse attention afterwards
@@ -187,7 +254,7 @@ def main():
     import torch
     import paper_2503_16428_amd as X
 
-    w = W.WORKLOADS[a.workload or ("c5" if a.dit_schedule else "c3")]
+    w = W.WORKLOADS[a.workload or ("c5" if a.dit_schedule else "c4" if a.sweep else "c3")]
     if a.stride is not None:
         w = w.with_(stride=a.stride)
     if a.tau is not None:
@@ -209,6 +276,9 @@ def main():
     stream = torch.cuda.current_stream()
     if a.dit_schedule:
         schedule_main(a, w, q, k, v, dims, stream)
+        return
+    if a.sweep:
+        sweep_main(a, w, q, k, v, dims, stream)
         return
     lo_hi = [float(t) for t in a.tau_heads.split(",")]
     tau_h = np.linspace(lo_hi[0], lo_hi[-1], w.hq).astype(np.float32)
