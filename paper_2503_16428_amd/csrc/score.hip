@@ -103,12 +103,16 @@ __global__ __launch_bounds__(kThreads, 1) void score_partials(
     offB[i] = (uint32_t)(((size_t)rb * S * kHeadDim + c * 8) * 2);
   }
   const uint32_t lds0 = XATTN_LDS_ADDR(lds);
+  // lane t holds the query sub-row paired with key sub-row t; read per chunk
+  // with v_readlane (a table lookup in kernel-argument memory would put a
+  // scalar load and its wait on every chunk's critical path)
+  const int qsub_lane = pairing.q[lane < S ? lane : 0];
   auto issue = [&](int ch) {
     const int kap0 = ch * KC;
     const int tsub = kap0 / kHeadDim, e0 = kap0 % kHeadDim;
     const uint32_t st = lds0 + (uint32_t)((ch % NSTAGE) * 2 * kStage * 2);
     const uint16_t* baseA = Kg + kap0;
-    const uint16_t* baseB = Qh + pairing.q[tsub] * kHeadDim + e0;
+    const uint16_t* baseB = Qh + __builtin_amdgcn_readlane(qsub_lane, tsub) * kHeadDim + e0;
 #pragma unroll
     for (int i = 0; i < kDmaPerOp; ++i) {
       const uint32_t row_lds = (uint32_t)((32 * wv + kDmaRows * i) * KC * 2);
