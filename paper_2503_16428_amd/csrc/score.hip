@@ -107,18 +107,24 @@ __global__ __launch_bounds__(kThreads, 1) void score_partials(
   // with v_readlane (a table lookup in kernel-argument memory would put a
   // scalar load and its wait on every chunk's critical path)
   const int qsub_lane = pairing.q[lane < S ? lane : 0];
-  auto issue = [&](int ch) {
+  // Loads of chunk ch: i-th pair (A, B) of this wave's kDmaPerOp row groups.
+  // src(ch) gives the two scalar bases, dma_pair issues one pair.
+  auto srcA = [&](int ch) -> const uint16_t* { return Kg + ch * KC; };
+  auto srcB = [&](int ch) -> const uint16_t* {
     const int kap0 = ch * KC;
-    const int tsub = kap0 / kHeadDim, e0 = kap0 % kHeadDim;
+    return Qh + __builtin_amdgcn_readlane(qsub_lane, kap0 / kHeadDim) * kHeadDim + kap0 % kHeadDim;
+  };
+  auto dma_pair = [&](int ch, const uint16_t* baseA, const uint16_t* baseB, int i) {
     const uint32_t st = lds0 + (uint32_t)((ch % NSTAGE) * 2 * kStage * 2);
-    const uint16_t* baseA = Kg + kap0;
-    const uint16_t* baseB = Qh + __builtin_amdgcn_readlane(qsub_lane, tsub) * kHeadDim + e0;
+    const uint32_t row_lds = (uint32_t)((32 * wv + kDmaRows * i) * KC * 2);
+    dma16(baseA, offA[i], st + row_lds);
+    dma16(baseB, offB[i], st + kStage * 2 + row_lds);
+  };
+  auto issue = [&](int ch) {
+    const uint16_t* baseA = srcA(ch);
+    const uint16_t* baseB = srcB(ch);
 #pragma unroll
-    for (int i = 0; i < kDmaPerOp; ++i) {
-      const uint32_t row_lds = (uint32_t)((32 * wv + kDmaRows * i) * KC * 2);
-      dma16(baseA, offA[i], st + row_lds);
-      dma16(baseB, offB[i], st + kStage * 2 + row_lds);
-    }
+    for (int i = 0; i < kDmaPerOp; ++i) dma_pair(ch, baseA, baseB, i);
   };
 
   f32x16 acc[4][2];
@@ -131,11 +137,14 @@ __global__ __launch_bounds__(kThreads, 1) void score_partials(
   // work of a causal layer); a per-MFMA skip would break the inner loop into
   // branches that serialise every LDS read with its MFMA.
   const uint32_t xa = (uint32_t)swz_row(lr);  // swizzle of this lane's rows (32 t, 64 wr: same)
-  auto compute = [&](int ch) {
+  // hook(ks) runs at the start of k-step ks (the two-stage pipeline spreads
+  // the next chunk's loads there)
+  auto compute = [&](int ch, auto hook) {
     const uint16_t* A = lds + (ch % NSTAGE) * 2 * kStage;
     const uint16_t* Bm = A + kStage;
 #pragma unroll
     for (int ks = 0; ks < KC / 16; ++ks) {
+      hook(ks);
       const uint32_t coff = (uint32_t)((((2 * ks + lh) ^ xa)) << 3);  // elements
       u32x4 bq[2];
 #pragma unroll
@@ -169,24 +178,47 @@ __global__ __launch_bounds__(kThreads, 1) void score_partials(
   // whose stage chunk ch + NSTAGE - 1 now refills), prefetch, compute ch.
   constexpr int kLoads = 2 * kDmaPerOp;
   static_assert(NCH >= NSTAGE && NSTAGE >= 2 && NSTAGE <= 4, "pipeline shape");
+  auto no_hook = [](int) {};
 #pragma unroll
   for (int c = 0; c < NSTAGE - 1; ++c) issue(c);
-  for (int ch = 0; ch < NCH - (NSTAGE - 2); ++ch) {
-    wait_vmcnt<kLoads * (NSTAGE - 2)>();
-    barrier_nofence();
-    if (ch + NSTAGE - 1 < NCH) issue(ch + NSTAGE - 1);
-    compute(ch);
-  }
-  // drain: the last NSTAGE - 2 chunks, each with fewer loads still in flight
-  if constexpr (NSTAGE >= 4) {
-    wait_vmcnt<kLoads>();
-    barrier_nofence();
-    compute(NCH - 2);
-  }
-  if constexpr (NSTAGE >= 3) {
-    wait_vmcnt<0>();
-    barrier_nofence();
-    compute(NCH - 1);
+  if constexpr (NSTAGE == 2) {
+    // The loads of chunk ch + 1 are spread over compute(ch), KC/16 k-steps
+    // taking kDmaPerOp / (KC/16) pairs each (a burst at the chunk start would
+    // stall the wave at issue). Past the last chunk, chunk NCH - 1 is loaded
+    // again into the free stage (in bounds, never read): no branch in the loop.
+    static_assert(kDmaPerOp % (KC / 16) == 0 || KC / 16 % kDmaPerOp == 0, "spread shape");
+    for (int ch = 0; ch < NCH; ++ch) {
+      wait_vmcnt<0>();
+      barrier_nofence();
+      const int nx = ch + 1 < NCH ? ch + 1 : NCH - 1;
+      const uint16_t* nA = srcA(nx);
+      const uint16_t* nB = srcB(nx);
+      constexpr int kPerStep = kDmaPerOp >= KC / 16 ? kDmaPerOp / (KC / 16) : 1;
+      compute(ch, [&](int ks) {
+#pragma unroll
+        for (int i = 0; i < kPerStep; ++i)
+          if (ks * kPerStep + i < kDmaPerOp) dma_pair(ch + 1, nA, nB, ks * kPerStep + i);
+      });
+    }
+    wait_vmcnt<0>();  // the extra loads land before the LDS is released
+  } else {
+    for (int ch = 0; ch < NCH - (NSTAGE - 2); ++ch) {
+      wait_vmcnt<kLoads * (NSTAGE - 2)>();
+      barrier_nofence();
+      if (ch + NSTAGE - 1 < NCH) issue(ch + NSTAGE - 1);
+      compute(ch, no_hook);
+    }
+    // drain: the last NSTAGE - 2 chunks, each with fewer loads still in flight
+    if constexpr (NSTAGE >= 4) {
+      wait_vmcnt<kLoads>();
+      barrier_nofence();
+      compute(NCH - 2, no_hook);
+    }
+    if constexpr (NSTAGE >= 3) {
+      wait_vmcnt<0>();
+      barrier_nofence();
+      compute(NCH - 1, no_hook);
+    }
   }
 
   // ---- epilogue per 32-row slab n: this lane owns reduced row R and 64 of the
