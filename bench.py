@@ -406,6 +406,8 @@ def main():
         print("# cpu baseline (oracle) ...", file=sys.stderr, flush=True)
         cpu = cpu_baseline(w, x, a.cpu_rows)
         cpu["seconds"] = round(cpu["seconds"], 2)
+        # the sample's rate extrapolated to the whole layer (same unit as value)
+        cpu["extrapolated_s_per_layer"] = round(dflops / (cpu["value"] * 1e12), 2)
         cpu["value"] = round(cpu["value"], 6)
 
     value = dflops / (ms_step * 1e-3) / 1e12
