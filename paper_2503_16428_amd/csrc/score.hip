@@ -184,15 +184,13 @@ __global__ __launch_bounds__(kThreads, 1) void score_partials(
   if constexpr (NSTAGE == 2) {
     // The loads of chunk ch + 1 are spread over compute(ch), KC/16 k-steps
     // taking kDmaPerOp / (KC/16) pairs each (a burst at the chunk start would
-    // stall the wave at issue). Past the last chunk, chunk NCH - 1 is loaded
-    // again into the free stage (in bounds, never read): no branch in the loop.
+    // stall the wave at issue); the last chunk is peeled (nothing to load).
     static_assert(kDmaPerOp % (KC / 16) == 0 || KC / 16 % kDmaPerOp == 0, "spread shape");
-    for (int ch = 0; ch < NCH; ++ch) {
+    for (int ch = 0; ch + 1 < NCH; ++ch) {
       wait_vmcnt<0>();
       barrier_nofence();
-      const int nx = ch + 1 < NCH ? ch + 1 : NCH - 1;
-      const uint16_t* nA = srcA(nx);
-      const uint16_t* nB = srcB(nx);
+      const uint16_t* nA = srcA(ch + 1);
+      const uint16_t* nB = srcB(ch + 1);
       constexpr int kPerStep = kDmaPerOp >= KC / 16 ? kDmaPerOp / (KC / 16) : 1;
       compute(ch, [&](int ks) {
 #pragma unroll
@@ -200,7 +198,9 @@ __global__ __launch_bounds__(kThreads, 1) void score_partials(
           if (ks * kPerStep + i < kDmaPerOp) dma_pair(ch + 1, nA, nB, ks * kPerStep + i);
       });
     }
-    wait_vmcnt<0>();  // the extra loads land before the LDS is released
+    wait_vmcnt<0>();
+    barrier_nofence();
+    compute(NCH - 1, no_hook);
   } else {
     for (int ch = 0; ch < NCH - (NSTAGE - 2); ++ch) {
       wait_vmcnt<kLoads * (NSTAGE - 2)>();
