@@ -24,14 +24,8 @@ namespace {
 
 constexpr int TM = 256;             // reduced rows (R) and columns (c) per workgroup tile
 constexpr int TSUB = 128;           // column sub-tile owning one (m, l) pair per row
-#ifndef XATTN_SCORE_KC
-#define XATTN_SCORE_KC 64
-#endif
-#ifndef XATTN_SCORE_NSTAGE
-#define XATTN_SCORE_NSTAGE 2
-#endif
-constexpr int KC = XATTN_SCORE_KC;          // reduced-K chunk per pipeline stage (32 or 64)
-constexpr int NSTAGE = XATTN_SCORE_NSTAGE;  // pipeline depth: NSTAGE - 1 chunks in flight
+constexpr int KC = 64;              // reduced-K chunk per pipeline stage (128-byte rows)
+constexpr int NSTAGE = 2;           // stages: one chunk computed while the next loads
 constexpr int kThreads = 512;       // 8 waves: 2 (columns) x 4 (rows), 128 c x 64 R each
 constexpr int kStage = TM * KC;     // bf16 elements of one operand in one stage
 constexpr int kCPR = KC / 8;        // 16-byte chunks per LDS row
@@ -71,74 +65,82 @@ __global__ __launch_bounds__(kThreads, 1) void score_partials(
   const int wv = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int wc = wv & 1, wr = wv >> 1;
 
-  // logical order: (kv head, row tile, column tile, query head in group)
-  const int w = xcd_remap(blockIdx.x, n_work);
+  // Persistent: each workgroup runs a sequence of tiles. Logical order
+  // (kv head, row tile, column tile, query head in group); XCD x (blockIdx %
+  // 8) takes one contiguous range of it, so the heads of a group that share
+  // K~ rows run on one L2. While the last chunk of a tile is computed, the
+  // first chunk of the next tile loads; its epilogue then overlaps that load.
+  const int x8 = blockIdx.x % kNumXcd, k8 = blockIdx.x / kNumXcd;
+  const int nper = gridDim.x / kNumXcd;  // workgroups per XCD (grid is a multiple of 8)
+  const int per = n_work / kNumXcd, rem = n_work % kNumXcd;
+  const int lo = x8 * per + (x8 < rem ? x8 : rem);
+  const int cnt_x = per + (x8 < rem ? 1 : 0);
   const int G = hq / hkv;
-  const int hh = w % G;
-  const int rest = w / G;
-  const int tile = rest % tiles_per_head;
-  const int gidx = rest / tiles_per_head;
-  const int h = (gidx / hkv) * hq + (gidx % hkv) * G + hh;
-  int rt, ct;
-  if (CAUSAL) {
-    tri_decode(tile, rt, ct);
-  } else {
-    rt = tile / ceil_div(NR, TM);
-    ct = tile % ceil_div(NR, TM);
-  }
-  const int R0 = rt * TM, c0 = ct * TM;
-  const uint16_t* Qh = q + (size_t)h * L * kHeadDim;
-  const uint16_t* Kg = k + (size_t)gidx * L * kHeadDim;
 
-  // ---- direct-to-LDS staging: per stage each wave loads rows 32 wv .. +32 of
-  // both operands, kDmaPerOp instructions (kDmaRows rows x 2 KC bytes) each.
-  // Rows beyond NR are clamped to NR - 1 (results masked / not stored).
+  // The tile being loaded: its head, first reduced row / column, operand
+  // bases (scalar) and this lane's load offsets. After a tile's last chunk
+  // load it is switched to the next tile, whose first chunk then loads while
+  // the finished tile (h_done, R0_done, c0_done) runs its epilogue.
+  int th = 0, tR0 = 0, tc0 = 0;
+  const uint16_t* tQh = q;
+  const uint16_t* tKg = k;
   uint32_t offA[kDmaPerOp], offB[kDmaPerOp];
+  auto load_tile = [&](int w) {
+    const int hh = w % G;
+    const int rest = w / G;
+    const int tile = rest % tiles_per_head;
+    const int gidx = rest / tiles_per_head;
+    th = __builtin_amdgcn_readfirstlane((gidx / hkv) * hq + (gidx % hkv) * G + hh);
+    int rt, ct;
+    if (CAUSAL) {
+      tri_decode(tile, rt, ct);
+    } else {
+      rt = tile / ceil_div(NR, TM);
+      ct = tile % ceil_div(NR, TM);
+    }
+    tR0 = __builtin_amdgcn_readfirstlane(rt * TM);
+    tc0 = __builtin_amdgcn_readfirstlane(ct * TM);
+    tQh = q + (size_t)th * L * kHeadDim;
+    tKg = k + (size_t)__builtin_amdgcn_readfirstlane(gidx) * L * kHeadDim;
+    // direct-to-LDS staging: per stage each wave loads rows 32 wv .. +32 of
+    // both operands, kDmaPerOp instructions (kDmaRows rows x 2 KC bytes)
+    // each; rows beyond NR are clamped to NR - 1 (results masked / not stored)
 #pragma unroll
-  for (int i = 0; i < kDmaPerOp; ++i) {
-    const int r = 32 * wv + kDmaRows * i + lane / kCPR;
-    const int c = (lane & (kCPR - 1)) ^ swz_row(r);
-    const int ra = min(c0 + r, NR - 1), rb = min(R0 + r, NR - 1);
-    offA[i] = (uint32_t)(((size_t)ra * KD + c * 8) * 2);
-    offB[i] = (uint32_t)(((size_t)rb * S * kHeadDim + c * 8) * 2);
-  }
+    for (int i = 0; i < kDmaPerOp; ++i) {
+      const int r = 32 * wv + kDmaRows * i + lane / kCPR;
+      const int c = (lane & (kCPR - 1)) ^ swz_row(r);
+      const int ra = min(tc0 + r, NR - 1), rb = min(tR0 + r, NR - 1);
+      offA[i] = (uint32_t)(((size_t)ra * KD + c * 8) * 2);
+      offB[i] = (uint32_t)(((size_t)rb * S * kHeadDim + c * 8) * 2);
+    }
+  };
+
   const uint32_t lds0 = XATTN_LDS_ADDR(lds);
   // lane t holds the query sub-row paired with key sub-row t; read per chunk
   // with v_readlane (a table lookup in kernel-argument memory would put a
   // scalar load and its wait on every chunk's critical path)
   const int qsub_lane = pairing.q[lane < S ? lane : 0];
-  // Loads of chunk ch: i-th pair (A, B) of this wave's kDmaPerOp row groups.
-  // src(ch) gives the two scalar bases, dma_pair issues one pair.
-  auto srcA = [&](int ch) -> const uint16_t* { return Kg + ch * KC; };
-  auto srcB = [&](int ch) -> const uint16_t* {
+  // Load pair i (operand A = K~ rows, B = Q~ rows) of chunk ch of tile t into
+  // stage ch % NSTAGE.
+  auto dma_pair = [&](int ch, int i) {
     const int kap0 = ch * KC;
-    return Qh + __builtin_amdgcn_readlane(qsub_lane, kap0 / kHeadDim) * kHeadDim + kap0 % kHeadDim;
-  };
-  auto dma_pair = [&](int ch, const uint16_t* baseA, const uint16_t* baseB, int i) {
+    const uint16_t* baseA = tKg + kap0;
+    const uint16_t* baseB =
+        tQh + __builtin_amdgcn_readlane(qsub_lane, kap0 / kHeadDim) * kHeadDim + kap0 % kHeadDim;
     const uint32_t st = lds0 + (uint32_t)((ch % NSTAGE) * 2 * kStage * 2);
     const uint32_t row_lds = (uint32_t)((32 * wv + kDmaRows * i) * KC * 2);
     dma16(baseA, offA[i], st + row_lds);
     dma16(baseB, offB[i], st + kStage * 2 + row_lds);
   };
-  auto issue = [&](int ch) {
-    const uint16_t* baseA = srcA(ch);
-    const uint16_t* baseB = srcB(ch);
-#pragma unroll
-    for (int i = 0; i < kDmaPerOp; ++i) dma_pair(ch, baseA, baseB, i);
-  };
 
   f32x16 acc[4][2];
-#pragma unroll
-  for (int t = 0; t < 4; ++t)
-#pragma unroll
-    for (int n = 0; n < 2; ++n) acc[t][n] = f32x16{};
 
   // Diagonal tiles are computed in full (their masked half is ~2% of the MFMA
   // work of a causal layer); a per-MFMA skip would break the inner loop into
   // branches that serialise every LDS read with its MFMA.
   const uint32_t xa = (uint32_t)swz_row(lr);  // swizzle of this lane's rows (32 t, 64 wr: same)
-  // hook(ks) runs at the start of k-step ks (the two-stage pipeline spreads
-  // the next chunk's loads there)
+  // hook(ks) runs at the start of k-step ks: the loads of the next chunk are
+  // spread over the k-steps (a burst after the barrier stalls the wave at issue)
   auto compute = [&](int ch, auto hook) {
     const uint16_t* A = lds + (ch % NSTAGE) * 2 * kStage;
     const uint16_t* Bm = A + kStage;
@@ -161,7 +163,7 @@ __global__ __launch_bounds__(kThreads, 1) void score_partials(
     // 8 MFMAs with the 6 reads of the next k-step interleaved.
     __builtin_amdgcn_sched_group_barrier(0x100, 6, 0);
 #pragma unroll
-    for (int k = 0; k + 1 < KC / 16; ++k) {
+    for (int kk = 0; kk + 1 < KC / 16; ++kk) {
 #pragma unroll
       for (int i = 0; i < 6; ++i) {
         __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
@@ -171,164 +173,147 @@ __global__ __launch_bounds__(kThreads, 1) void score_partials(
     }
     __builtin_amdgcn_sched_group_barrier(0x008, 8, 0);
   };
+  static_assert(kDmaPerOp == KC / 16, "one load pair per k-step");
 
-  // Each wave issues L = 2 kDmaPerOp loads per chunk (NCH = S d / KC >= NSTAGE).
-  // Step ch: wait for chunk ch (the next NSTAGE - 2 chunks may stay in
-  // flight), one barrier (chunk ch visible; every wave finished chunk ch - 1,
-  // whose stage chunk ch + NSTAGE - 1 now refills), prefetch, compute ch.
-  constexpr int kLoads = 2 * kDmaPerOp;
-  static_assert(NCH >= NSTAGE && NSTAGE >= 2 && NSTAGE <= 4, "pipeline shape");
-  auto no_hook = [](int) {};
+  auto epilogue = [&](const int h, const int R0, const int c0) {
+    // ---- epilogue per 32-row slab n: this lane owns reduced row R and 64 of the
+    // wave's 128 columns; lane (lr, 1-lh) owns the other 64.
+    const int csub = c0 + 128 * wc;  // first column of this wave's sub-tile
+    const int tsub_idx = csub / TSUB;
+    const int j0 = csub / NRB;
+  #pragma unroll
+    for (int n = 0; n < 2; ++n) {
+      const int R = R0 + 64 * wr + 32 * n + lr;
+      // Invalid columns (c > R when causal, c >= NR) occur only in sub-tiles
+      // that reach past the slab's first row or the reduced length; the empty
+      // asm keeps this uniform branch from becoming selects on every tile.
+      const int Rslab = R0 + 64 * wr + 32 * n;
+      if ((CAUSAL && csub + 127 > Rslab) || csub + 127 >= NR) {
+        asm volatile("");
+  #pragma unroll
+        for (int t = 0; t < 4; ++t) {
+  #pragma unroll
+          for (int r = 0; r < 16; ++r) {
+            const int c = csub + 32 * t + 8 * (r >> 2) + 4 * lh + (r & 3);
+            if (c >= NR || (CAUSAL && c > R)) acc[t][n][r] = -INFINITY;
+          }
+        }
+      }
+      // max of the raw products (the scale is positive), then every term as
+      // one fma inside the exponential: p = 2^(x scale - m)
+      float mloc = -INFINITY;
+  #pragma unroll
+      for (int t = 0; t < 4; ++t) {
+  #pragma unroll
+        for (int r = 0; r < 16; ++r) mloc = fmaxf(mloc, acc[t][n][r]);
+      }
+      const float m = fmaxf(mloc, __shfl_xor(mloc, 32)) * scale_log2;
+      const float mref = (m == -INFINITY) ? 0.f : m;
+      float gsum[16];  // groups of 4 consecutive columns: group gi = 4 t + r / 4
+      float lloc = 0.f;
+  #pragma unroll
+      for (int t = 0; t < 4; ++t) {
+  #pragma unroll
+        for (int g4 = 0; g4 < 4; ++g4) {
+          float sum = 0.f;
+  #pragma unroll
+          for (int e = 0; e < 4; ++e) {
+            const float p = fast_exp2(fmaf(acc[t][n][4 * g4 + e], scale_log2, -mref));
+            acc[t][n][4 * g4 + e] = p;
+            sum += p;
+          }
+          gsum[4 * t + g4] = sum;
+          lloc += sum;
+        }
+      }
+      const float l = lloc + __shfl_xor(lloc, 32);
+      const bool rvalid = R < NR;
+      // part is [head][query block][key block][row in block]: what the
+      // finalize workgroup of one query block reads is one contiguous slab;
+      // a half-wave writes 32 / NRB runs of NRB consecutive floats per block.
+      const int Rv = rvalid ? R : 0;
+      float* pcol = part + ((size_t)(h * NB + Rv / NRB) * NB) * NRB + (Rv % NRB);
+  
+      if constexpr (NRB >= 8) {
+        // group gi covers columns 8 gi + 4 lh + [0, 4): local block gi / (NRB / 8)
+        constexpr int GPB = NRB / 8;
+        constexpr int NBL = TSUB / NRB;
+        float pb[NBL];
+  #pragma unroll
+        for (int jb = 0; jb < NBL; ++jb) {
+          float sum = 0.f;
+  #pragma unroll
+          for (int x = 0; x < GPB; ++x) sum += gsum[jb * GPB + x];
+          pb[jb] = sum + __shfl_xor(sum, 32);
+        }
+        if (rvalid) {
+          if constexpr (NBL >= 2) {
+  #pragma unroll
+            for (int x = 0; x < NBL / 2; ++x) {
+              const int jb = lh * (NBL / 2) + x;
+              if (j0 + jb < NB) pcol[(size_t)(j0 + jb) * NRB] = pb[jb];
+            }
+          } else {
+            if (lh == 0 && j0 < NB) pcol[(size_t)j0 * NRB] = pb[0];
+          }
+        }
+      } else if constexpr (NRB == 4) {
+        // each group of 4 columns is one block: local block 2 gi + lh
+        if (rvalid) {
+  #pragma unroll
+          for (int gi = 0; gi < 16; ++gi) {
+            const int j = j0 + 2 * gi + lh;
+            if (j < NB) pcol[(size_t)j * NRB] = gsum[gi];
+          }
+        }
+      } else {  // NRB == 2: each group holds two blocks
+        static_assert(NRB == 2, "stride must divide the block");
+        if (rvalid) {
+  #pragma unroll
+          for (int t = 0; t < 4; ++t) {
+  #pragma unroll
+            for (int g4 = 0; g4 < 4; ++g4) {
+              const int gi = 4 * t + g4;
+              const int j = j0 + 4 * gi + 2 * lh;
+              if (j < NB) pcol[(size_t)j * NRB] = acc[t][n][4 * g4] + acc[t][n][4 * g4 + 1];
+              if (j + 1 < NB) pcol[(size_t)(j + 1) * NRB] = acc[t][n][4 * g4 + 2] + acc[t][n][4 * g4 + 3];
+            }
+          }
+        }
+      }
+      if (rvalid && lh == 0 && tsub_idx < NT)
+        stats[((size_t)h * NT + tsub_idx) * NR + R] = make_float2(m, l);
+    }
+  };
+
+  if (cnt_x <= k8) return;  // no tile for this workgroup (uniform)
+  load_tile(lo + k8);
 #pragma unroll
-  for (int c = 0; c < NSTAGE - 1; ++c) issue(c);
-  if constexpr (NSTAGE == 2) {
-    // The loads of chunk ch + 1 are spread over compute(ch), KC/16 k-steps
-    // taking kDmaPerOp / (KC/16) pairs each (a burst at the chunk start would
-    // stall the wave at issue); the last chunk is peeled (nothing to load).
-    static_assert(kDmaPerOp % (KC / 16) == 0 || KC / 16 % kDmaPerOp == 0, "spread shape");
+  for (int i = 0; i < kDmaPerOp; ++i) dma_pair(0, i);
+  for (int it = k8; it < cnt_x; it += nper) {
+#pragma unroll
+    for (int t = 0; t < 4; ++t)
+#pragma unroll
+      for (int n = 0; n < 2; ++n) acc[t][n] = f32x16{};
+    // Step ch: this wave's loads of chunk ch have landed; the barrier makes
+    // everyone's visible and ends every wave's reads of chunk ch - 1, whose
+    // stage now receives chunk ch + 1, one pair per k-step of compute(ch).
     for (int ch = 0; ch + 1 < NCH; ++ch) {
       wait_vmcnt<0>();
       barrier_nofence();
-      const uint16_t* nA = srcA(ch + 1);
-      const uint16_t* nB = srcB(ch + 1);
-      constexpr int kPerStep = kDmaPerOp >= KC / 16 ? kDmaPerOp / (KC / 16) : 1;
-      compute(ch, [&](int ks) {
-#pragma unroll
-        for (int i = 0; i < kPerStep; ++i)
-          if (ks * kPerStep + i < kDmaPerOp) dma_pair(ch + 1, nA, nB, ks * kPerStep + i);
-      });
+      compute(ch, [&](int ks) { dma_pair(ch + 1, ks); });
     }
     wait_vmcnt<0>();
     barrier_nofence();
-    compute(NCH - 1, no_hook);
-  } else {
-    for (int ch = 0; ch < NCH - (NSTAGE - 2); ++ch) {
-      wait_vmcnt<kLoads * (NSTAGE - 2)>();
-      barrier_nofence();
-      if (ch + NSTAGE - 1 < NCH) issue(ch + NSTAGE - 1);
-      compute(ch, no_hook);
-    }
-    // drain: the last NSTAGE - 2 chunks, each with fewer loads still in flight
-    if constexpr (NSTAGE >= 4) {
-      wait_vmcnt<kLoads>();
-      barrier_nofence();
-      compute(NCH - 2, no_hook);
-    }
-    if constexpr (NSTAGE >= 3) {
-      wait_vmcnt<0>();
-      barrier_nofence();
-      compute(NCH - 1, no_hook);
-    }
+    // Chunk 0 of the next tile goes to stage 0 (chunk NCH - 2's, finished by
+    // everyone) during the last chunk; after the last tile the same tile's
+    // chunk 0 is loaded again (in bounds, never read).
+    const int h_done = th, R0_done = tR0, c0_done = tc0;
+    if (it + nper < cnt_x) load_tile(lo + it + nper);
+    compute(NCH - 1, [&](int ks) { dma_pair(0, ks); });
+    epilogue(h_done, R0_done, c0_done);
   }
-
-  // ---- epilogue per 32-row slab n: this lane owns reduced row R and 64 of the
-  // wave's 128 columns; lane (lr, 1-lh) owns the other 64.
-  const int csub = c0 + 128 * wc;  // first column of this wave's sub-tile
-  const int tsub_idx = csub / TSUB;
-  const int j0 = csub / NRB;
-#pragma unroll
-  for (int n = 0; n < 2; ++n) {
-    const int R = R0 + 64 * wr + 32 * n + lr;
-    // Invalid columns (c > R when causal, c >= NR) occur only in sub-tiles
-    // that reach past the slab's first row or the reduced length; the empty
-    // asm keeps this uniform branch from becoming selects on every tile.
-    const int Rslab = R0 + 64 * wr + 32 * n;
-    if ((CAUSAL && csub + 127 > Rslab) || csub + 127 >= NR) {
-      asm volatile("");
-#pragma unroll
-      for (int t = 0; t < 4; ++t) {
-#pragma unroll
-        for (int r = 0; r < 16; ++r) {
-          const int c = csub + 32 * t + 8 * (r >> 2) + 4 * lh + (r & 3);
-          if (c >= NR || (CAUSAL && c > R)) acc[t][n][r] = -INFINITY;
-        }
-      }
-    }
-    // max of the raw products (the scale is positive), then every term as
-    // one fma inside the exponential: p = 2^(x scale - m)
-    float mloc = -INFINITY;
-#pragma unroll
-    for (int t = 0; t < 4; ++t) {
-#pragma unroll
-      for (int r = 0; r < 16; ++r) mloc = fmaxf(mloc, acc[t][n][r]);
-    }
-    const float m = fmaxf(mloc, __shfl_xor(mloc, 32)) * scale_log2;
-    const float mref = (m == -INFINITY) ? 0.f : m;
-    float gsum[16];  // groups of 4 consecutive columns: group gi = 4 t + r / 4
-    float lloc = 0.f;
-#pragma unroll
-    for (int t = 0; t < 4; ++t) {
-#pragma unroll
-      for (int g4 = 0; g4 < 4; ++g4) {
-        float sum = 0.f;
-#pragma unroll
-        for (int e = 0; e < 4; ++e) {
-          const float p = fast_exp2(fmaf(acc[t][n][4 * g4 + e], scale_log2, -mref));
-          acc[t][n][4 * g4 + e] = p;
-          sum += p;
-        }
-        gsum[4 * t + g4] = sum;
-        lloc += sum;
-      }
-    }
-    const float l = lloc + __shfl_xor(lloc, 32);
-    const bool rvalid = R < NR;
-    // part is [head][query block][key block][row in block]: what the
-    // finalize workgroup of one query block reads is one contiguous slab;
-    // a half-wave writes 32 / NRB runs of NRB consecutive floats per block.
-    const int Rv = rvalid ? R : 0;
-    float* pcol = part + ((size_t)(h * NB + Rv / NRB) * NB) * NRB + (Rv % NRB);
-
-    if constexpr (NRB >= 8) {
-      // group gi covers columns 8 gi + 4 lh + [0, 4): local block gi / (NRB / 8)
-      constexpr int GPB = NRB / 8;
-      constexpr int NBL = TSUB / NRB;
-      float pb[NBL];
-#pragma unroll
-      for (int jb = 0; jb < NBL; ++jb) {
-        float sum = 0.f;
-#pragma unroll
-        for (int x = 0; x < GPB; ++x) sum += gsum[jb * GPB + x];
-        pb[jb] = sum + __shfl_xor(sum, 32);
-      }
-      if (rvalid) {
-        if constexpr (NBL >= 2) {
-#pragma unroll
-          for (int x = 0; x < NBL / 2; ++x) {
-            const int jb = lh * (NBL / 2) + x;
-            if (j0 + jb < NB) pcol[(size_t)(j0 + jb) * NRB] = pb[jb];
-          }
-        } else {
-          if (lh == 0 && j0 < NB) pcol[(size_t)j0 * NRB] = pb[0];
-        }
-      }
-    } else if constexpr (NRB == 4) {
-      // each group of 4 columns is one block: local block 2 gi + lh
-      if (rvalid) {
-#pragma unroll
-        for (int gi = 0; gi < 16; ++gi) {
-          const int j = j0 + 2 * gi + lh;
-          if (j < NB) pcol[(size_t)j * NRB] = gsum[gi];
-        }
-      }
-    } else {  // NRB == 2: each group holds two blocks
-      static_assert(NRB == 2, "stride must divide the block");
-      if (rvalid) {
-#pragma unroll
-        for (int t = 0; t < 4; ++t) {
-#pragma unroll
-          for (int g4 = 0; g4 < 4; ++g4) {
-            const int gi = 4 * t + g4;
-            const int j = j0 + 4 * gi + 2 * lh;
-            if (j < NB) pcol[(size_t)j * NRB] = acc[t][n][4 * g4] + acc[t][n][4 * g4 + 1];
-            if (j + 1 < NB) pcol[(size_t)(j + 1) * NRB] = acc[t][n][4 * g4 + 2] + acc[t][n][4 * g4 + 3];
-          }
-        }
-      }
-    }
-    if (rvalid && lh == 0 && tsub_idx < NT)
-      stats[((size_t)h * NT + tsub_idx) * NR + R] = make_float2(m, l);
-  }
+  wait_vmcnt<0>();  // the last loads land before the LDS is released
 }
 
 __device__ __forceinline__ float wave_max(float x) {
@@ -457,6 +442,22 @@ __global__ __launch_bounds__(256) void score_finalize(const float* __restrict__ 
   for (int j = ncand + tid; j < NB; j += 256) out[j] = 0.f;  // not candidates
 }
 
+// Compute units of the current device, rounded down to a multiple of the 8
+// XCDs (cached per device).
+int persistent_workgroups() {
+  static int cached[64] = {};
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) dev = 0;
+  if (cached[dev] == 0) {
+    int cus = 0;
+    if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
+        cus < kNumXcd)
+      cus = 256;
+    cached[dev] = cus / kNumXcd * kNumXcd;
+  }
+  return cached[dev];
+}
+
 template <int NRB, bool CAUSAL>
 hipError_t launch_partials(const void* q, const void* k, const XattnShape& s,
                            const SubRowPairing& pr, float* part, float* stats, hipStream_t st) {
@@ -465,7 +466,9 @@ hipError_t launch_partials(const void* q, const void* k, const XattnShape& s,
   const int tiles = CAUSAL ? T * (T + 1) / 2 : T * T;
   const int n_work = s.batch * s.hkv * tiles * (s.hq / s.hkv);
   const float scale_log2 = kLog2e / (sqrtf((float)kHeadDim) * (float)S);
-  hipLaunchKernelGGL((score_partials<NRB, CAUSAL>), dim3(n_work), dim3(kThreads), 0, st,
+  // one resident workgroup per CU (128 KB of LDS each), a multiple of 8
+  const int wgs = persistent_workgroups();
+  hipLaunchKernelGGL((score_partials<NRB, CAUSAL>), dim3(wgs), dim3(kThreads), 0, st,
                      (const uint16_t*)q, (const uint16_t*)k, s.hq, s.hkv, s.seq, NR, NB, NT,
                      tiles, n_work, scale_log2, pr, part, (float2*)stats);
   return hipGetLastError();
