@@ -248,7 +248,7 @@ def schedule_main(a, w, q, k, v, dims, stream):
 def main():
     a = parse()
     if a.gpus != 1:
-        print(json.dumps({"error": "this build runs on exactly one GPU; multi-GPU runs are "
+        print(json.dumps({"error": "this benchmark runs on exactly one GPU; multi-GPU runs are "
                                    "not part of it (--gpus must be 1)"}), flush=True)
         sys.exit(2)
     import torch
