@@ -39,6 +39,9 @@ def parse():
     ap.add_argument("--workload", default=None, choices=sorted(W.WORKLOADS),
                     help="default c3 (c5 with --dit-schedule)")
     ap.add_argument("--stride", type=int, default=None)
+    ap.add_argument("--seq", type=int, default=None,
+                    help="override the workload's sequence length (a multiple of 128, at "
+                         "most 262144); the name records it")
     ap.add_argument("--tau", type=float, default=None)
     ap.add_argument("--select-mode", default="threshold",
                     choices=["threshold", "heads", "topk", "ratio"],
@@ -255,6 +258,8 @@ def main():
     import paper_2503_16428_amd as X
 
     w = W.WORKLOADS[a.workload or ("c5" if a.dit_schedule else "c4" if a.sweep else "c3")]
+    if a.seq is not None:
+        w = w.with_(seq=a.seq, name=f"{w.name}_seq{a.seq}")
     if a.stride is not None:
         w = w.with_(stride=a.stride)
     if a.tau is not None:
