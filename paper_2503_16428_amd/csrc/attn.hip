@@ -51,6 +51,17 @@ __device__ __forceinline__ float half_max(float x) {
   return fmaxf(__builtin_bit_cast(float, (uint32_t)r[0]), __builtin_bit_cast(float, (uint32_t)r[1]));
 }
 
+// this lane's max over the 32 scores of a half-tile
+__device__ __forceinline__ float lane_max(const f32x16 (&s)[2]) {
+  float m = -INFINITY;
+#pragma unroll
+  for (int kt = 0; kt < 2; ++kt) {
+#pragma unroll
+    for (int r = 0; r < 16; ++r) m = fmaxf(m, s[kt][r]);
+  }
+  return m;
+}
+
 __device__ __forceinline__ uint32_t cvt_pk_bf16(float a, float b) {
   return __builtin_bit_cast(uint32_t, __builtin_convertvector(f32v2{a, b}, bf16v2));
 }
@@ -201,7 +212,8 @@ __device__ __forceinline__ void attn_body(
   // buffer of i and V(i+1) into the other V buffer, computes S(i+1) into sn
   // (from stale data on the last step: never used) and accumulates PV(i).
   // PAR fixes the buffers at compile time (the loop is unrolled by 2).
-  auto step = [&](auto par_tag, bool has_next, int jn, f32x16 (&sc)[2], f32x16 (&sn)[2]) {
+  auto step = [&](auto par_tag, bool has_next, int jn, f32x16 (&sc)[2], f32x16 (&sn)[2],
+                  float& mpre) {
     constexpr int PAR = decltype(par_tag)::value;
     const int key0 = jc * kBlock + PAR * kHalf;
     wait_vmcnt<0>();    // this wave's loads of K(i+1) and V(i) have landed
@@ -226,6 +238,9 @@ __device__ __forceinline__ void attn_body(
 
     // causal mask: only half-tiles reaching past this wave's first query (the
     // empty asm keeps this uniform branch from becoming selects on every step)
+    // (mpre is this lane's max of sc, taken during the previous step; on
+    // masked half-tiles it is taken again here)
+    float mraw = mpre;
     if (CAUSAL && key0 + kHalf - 1 > q0) {
       asm volatile("");
 #pragma unroll
@@ -236,12 +251,7 @@ __device__ __forceinline__ void attn_body(
           if (key > qi) sc[kt][r] = -INFINITY;
         }
       }
-    }
-    float mraw = -INFINITY;
-#pragma unroll
-    for (int kt = 0; kt < 2; ++kt) {
-#pragma unroll
-      for (int r = 0; r < 16; ++r) mraw = fmaxf(mraw, sc[kt][r]);
+      mraw = lane_max(sc);
     }
     mraw = half_max(mraw);
     const float mt = mraw * scale_log2;  // scale > 0: max commutes with it
@@ -296,22 +306,34 @@ __device__ __forceinline__ void attn_body(
         oacc[dt] = mfma32(as_bf16x8(u32x4{lo2[0], lo2[1], hi2[0], hi2[1]}), pb, oacc[dt]);
       }
     }
-    // Schedule: LDS reads run two MFMAs ahead of their use; each QK^T MFMA
-    // carries 5 VALU and 2 transcendental instructions of the softmax; the
-    // first PV operands are read during the last QK^T MFMAs.
+    mpre = lane_max(sn);  // for the next step, beside the last PV MFMAs
+    asm volatile("" ::"v"(mpre));  // (not sunk past the next step's mask branch)
+    // Schedule: LDS reads run two MFMAs ahead of their use. The softmax work
+    // is spread over all 32 MFMAs so that no MFMA waits for more than its own
+    // 32 cycles of VALU (an exp2 issues in 16, other VALU in 4): the QK^T
+    // MFMAs carry the exponentials of PV steps 0-2 (1.5 per MFMA, with their
+    // fma / add / convert), the first 8 PV MFMAs those of PV step 3, the last
+    // 8 the max of S(i+1).
     __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);    // DS read (K operand)
 #pragma unroll
     for (int t = 0; t < 16; ++t) {
       __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // QK^T MFMA
       __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);  // DS read
       if (t >= 14) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
-      __builtin_amdgcn_sched_group_barrier(0x002, 5, 0);  // VALU
-      __builtin_amdgcn_sched_group_barrier(0x400, 2, 0);  // exp2
+      __builtin_amdgcn_sched_group_barrier(0x002, 4, 0);  // VALU
+      if (t & 1) __builtin_amdgcn_sched_group_barrier(0x400, 1, 0);  // exp2
+      else __builtin_amdgcn_sched_group_barrier(0x400, 2, 0);
     }
 #pragma unroll
     for (int t = 0; t < 16; ++t) {
       __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // PV MFMA
       if (t < 14) __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);  // DS transpose reads
+      if (t < 8) {
+        __builtin_amdgcn_sched_group_barrier(0x002, 3, 0);
+        __builtin_amdgcn_sched_group_barrier(0x400, 1, 0);
+      } else {
+        __builtin_amdgcn_sched_group_barrier(0x002, 2, 0);
+      }
     }
   };
 
@@ -320,11 +342,12 @@ __device__ __forceinline__ void attn_body(
     wait_vmcnt<0>();
     barrier_nofence();
     qk(0, sa, [](int) {});
+    float mpre = lane_max(sa);
     for (int p = 0; p < n_kb; ++p) {
       const bool has_next = p + 1 < n_kb;
       const int jn = has_next ? block_at(p + 1) : jc;
-      step(std::integral_constant<int, 0>{}, has_next, jn, sa, sb);
-      step(std::integral_constant<int, 1>{}, has_next, jn, sb, sa);
+      step(std::integral_constant<int, 0>{}, has_next, jn, sa, sb, mpre);
+      step(std::integral_constant<int, 1>{}, has_next, jn, sb, sa, mpre);
       jc = jn;
     }
     wait_vmcnt<0>();  // the last prefetches land before the LDS is released
