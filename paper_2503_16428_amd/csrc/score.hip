@@ -49,6 +49,15 @@ __device__ __forceinline__ void tri_decode(int t, int& rt, int& ct) {
 // one logical chunk hit 16 distinct bank groups.
 __device__ __forceinline__ int swz_row(int r) { return (r / kRowsPer256) & (kCPR - 1); }
 
+// Lane l < 32 returns a[l] + a[l + 32]; lane l >= 32 returns b[l - 32] + b[l]
+// (one v_permlane32_swap exchanges the upper half of a with the lower half of
+// b).
+__device__ __forceinline__ float half_pair_sum(float a, float b) {
+  const auto r = __builtin_amdgcn_permlane32_swap(__builtin_bit_cast(uint32_t, a),
+                                                  __builtin_bit_cast(uint32_t, b), false, false);
+  return __builtin_bit_cast(float, (uint32_t)r[0]) + __builtin_bit_cast(float, (uint32_t)r[1]);
+}
+
 // NRB = reduced rows (and columns) per 128-token block = 128 / S.
 template <int NRB, bool CAUSAL>
 __global__ __launch_bounds__(kThreads, 1) void score_partials(
@@ -238,24 +247,26 @@ __global__ __launch_bounds__(kThreads, 1) void score_partials(
         // group gi covers columns 8 gi + 4 lh + [0, 4): local block gi / (NRB / 8)
         constexpr int GPB = NRB / 8;
         constexpr int NBL = TSUB / NRB;
-        float pb[NBL];
-  #pragma unroll
-        for (int jb = 0; jb < NBL; ++jb) {
+        auto block_sum = [&](int jb) {
           float sum = 0.f;
   #pragma unroll
           for (int x = 0; x < GPB; ++x) sum += gsum[jb * GPB + x];
-          pb[jb] = sum + __shfl_xor(sum, 32);
-        }
-        if (rvalid) {
-          if constexpr (NBL >= 2) {
+          return sum;
+        };
+        if constexpr (NBL >= 2) {
+          // blocks x and NBL/2 + x in one exchange: lanes < 32 end up with
+          // block x's total over both column halves, lanes >= 32 with block
+          // NBL/2 + x's, each the one it stores
   #pragma unroll
-            for (int x = 0; x < NBL / 2; ++x) {
-              const int jb = lh * (NBL / 2) + x;
-              if (j0 + jb < NB) pcol[(size_t)(j0 + jb) * NRB] = pb[jb];
-            }
-          } else {
-            if (lh == 0 && j0 < NB) pcol[(size_t)j0 * NRB] = pb[0];
+          for (int x = 0; x < NBL / 2; ++x) {
+            const float tot = half_pair_sum(block_sum(x), block_sum(NBL / 2 + x));
+            const int jb = lh * (NBL / 2) + x;
+            if (rvalid && j0 + jb < NB) pcol[(size_t)(j0 + jb) * NRB] = tot;
           }
+        } else {
+          const float s0 = block_sum(0);
+          const float tot = half_pair_sum(s0, s0);
+          if (rvalid && lh == 0 && j0 < NB) pcol[(size_t)j0 * NRB] = tot;
         }
       } else if constexpr (NRB == 4) {
         // each group of 4 columns is one block: local block 2 gi + lh
