@@ -14,7 +14,7 @@
 // epilogue, per reduced row R and 128-column sub-tile t: the sub-tile max m
 // (log2 domain), l = sum exp2(x - m), and per key block j the partial mass
 // sum_{c in j} exp2(x - m). Kernel score_finalize
-// merges the tiles of each row (m_R = max_t m, l_R = sum_t l e^(m - m_R)),
+// merges the tiles of each row (m_R = max_t m, l_R = sum_t l 2^(m - m_R)),
 // normalises, and averages the B/S reduced rows of each query block.
 #include "common.h"
 
