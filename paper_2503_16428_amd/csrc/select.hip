@@ -15,7 +15,9 @@
 // The shortest prefix of the (u desc, j asc) order that reaches the target is
 // then every block with u_j > v* plus the first ceil((target - F(v*+1)) / v*)
 // blocks with u_j == v* in ascending j. Emitting in ascending j with ballot /
-// popcount yields the index list already sorted.
+// popcount yields the index list already sorted. After the first search steps
+// the few values still inside the search interval are gathered one per lane,
+// so the remaining steps no longer scan every candidate.
 #include "common.h"
 
 using namespace xattn;
@@ -41,6 +43,8 @@ __device__ __forceinline__ uint64_t wave_sum_u64(uint64_t x) {
   return ((uint64_t)hi << 21) + lo;
 }
 
+constexpr int kFullSteps = 10;  // search steps over every value before narrowing
+
 // One row with at most 64 NPL candidates; lane l holds j = l + 64 i. Every
 // per-lane partial sum below is at most NPL * 2^32 <= 2^37.
 //   COUNT = false (find_blocks): target = ceil(tau * T), F(v) = sum_{u >= v} u.
@@ -50,7 +54,8 @@ __device__ __forceinline__ uint64_t wave_sum_u64(uint64_t x) {
 template <int NPL, bool COUNT>
 __device__ __forceinline__ void select_row(const float* __restrict__ s, int m, float tau,
                                            int k, int lane, int32_t* __restrict__ out,
-                                           int32_t* __restrict__ cnt_out) {
+                                           int32_t* __restrict__ cnt_out,
+                                           uint64_t* __restrict__ stage) {
   uint64_t u[NPL];
   uint64_t tl = 0;
 #pragma unroll
@@ -88,10 +93,49 @@ __device__ __forceinline__ void select_row(const float* __restrict__ s, int m, f
 
   // largest v in [0, 2^32] with F(v) >= target; F(0) >= target, F(2^32 + 1) = 0
   uint64_t lo = 0, hi = (1ull << 32) + 1;
-  while (hi - lo > 1) {
+  for (int it = 0; it < kFullSteps && hi - lo > 1; ++it) {
     const uint64_t mid = (lo + hi) >> 1;
     if (F(mid, false) >= target) lo = mid;
     else hi = mid;
+  }
+  if (hi - lo > 1) {
+    // For v in (lo, hi) only the values in [lo, hi) can change F(v): F(v) =
+    // A + sum of those >= v, A = F(hi). When at most 64 remain they are
+    // gathered one per lane (through LDS) and the search ends on them alone,
+    // visiting the same midpoints with the same F values.
+    uint64_t a = 0;
+    uint32_t n = 0;
+#pragma unroll
+    for (int i = 0; i < NPL; ++i) {
+      a += u[i] >= hi ? (COUNT ? 1 : u[i]) : 0;
+      n += (lane + 64 * i < m && u[i] >= lo && u[i] < hi) ? 1u : 0u;
+    }
+    if (NPL > 2 && wave_sum_u32(n) <= 64) {
+      const uint64_t A = wave_sum_u64(a);
+      const uint64_t below = (1ull << lane) - 1ull;
+      uint32_t pos = 0;
+#pragma unroll
+      for (int i = 0; i < NPL; ++i) {
+        const bool in = lane + 64 * i < m && u[i] >= lo && u[i] < hi;
+        const uint64_t msk = __ballot(in);
+        if (in) stage[pos + __popcll(msk & below)] = u[i];
+        pos += __popcll(msk);
+      }
+      __builtin_amdgcn_wave_barrier();
+      const uint64_t c = lane < (int)pos ? stage[lane] : 0;  // 0 never counts: v >= 1
+      while (hi - lo > 1) {
+        const uint64_t mid = (lo + hi) >> 1;
+        const uint64_t f = A + wave_sum_u64(c >= mid ? (COUNT ? 1 : c) : 0);
+        if (f >= target) lo = mid;
+        else hi = mid;
+      }
+    } else {
+      while (hi - lo > 1) {
+        const uint64_t mid = (lo + hi) >> 1;
+        if (F(mid, false) >= target) lo = mid;
+        else hi = mid;
+      }
+    }
   }
   const uint64_t vstar = lo;
   const uint64_t base = F(vstar, true);  // < target by maximality of v*
@@ -118,14 +162,15 @@ __device__ __forceinline__ void select_row(const float* __restrict__ s, int m, f
 
 template <int NPL, bool COUNT>
 __device__ __forceinline__ void select_row_sized(const float* s, int m, float tau, int k,
-                                                 int lane, int32_t* out, int32_t* cnt_out) {
+                                                 int lane, int32_t* out, int32_t* cnt_out,
+                                                 uint64_t* stage) {
   const int nact = (m + 63) >> 6;
-  if (NPL <= 1 || nact <= 1) select_row<1, COUNT>(s, m, tau, k, lane, out, cnt_out);
-  else if (NPL <= 2 || nact <= 2) select_row<(NPL < 2 ? NPL : 2), COUNT>(s, m, tau, k, lane, out, cnt_out);
-  else if (NPL <= 4 || nact <= 4) select_row<(NPL < 4 ? NPL : 4), COUNT>(s, m, tau, k, lane, out, cnt_out);
-  else if (NPL <= 8 || nact <= 8) select_row<(NPL < 8 ? NPL : 8), COUNT>(s, m, tau, k, lane, out, cnt_out);
-  else if (NPL <= 16 || nact <= 16) select_row<(NPL < 16 ? NPL : 16), COUNT>(s, m, tau, k, lane, out, cnt_out);
-  else select_row<NPL, COUNT>(s, m, tau, k, lane, out, cnt_out);
+  if (NPL <= 1 || nact <= 1) select_row<1, COUNT>(s, m, tau, k, lane, out, cnt_out, stage);
+  else if (NPL <= 2 || nact <= 2) select_row<(NPL < 2 ? NPL : 2), COUNT>(s, m, tau, k, lane, out, cnt_out, stage);
+  else if (NPL <= 4 || nact <= 4) select_row<(NPL < 4 ? NPL : 4), COUNT>(s, m, tau, k, lane, out, cnt_out, stage);
+  else if (NPL <= 8 || nact <= 8) select_row<(NPL < 8 ? NPL : 8), COUNT>(s, m, tau, k, lane, out, cnt_out, stage);
+  else if (NPL <= 16 || nact <= 16) select_row<(NPL < 16 ? NPL : 16), COUNT>(s, m, tau, k, lane, out, cnt_out, stage);
+  else select_row<NPL, COUNT>(s, m, tau, k, lane, out, cnt_out, stage);
 }
 
 // One wave64 per (head, query block) row. NPL = slots per lane for the
@@ -137,6 +182,7 @@ __global__ __launch_bounds__(256) void select_kernel(const float* __restrict__ s
                                                      int n_rows, int NB, SelectParams p,
                                                      int32_t* __restrict__ idx,
                                                      int32_t* __restrict__ cnt) {
+  __shared__ uint64_t stage_all[4][64];  // per wave: the values left for the search's end
   const int lane = threadIdx.x & 63;
   const int row = blockIdx.x * 4 + (threadIdx.x >> 6);
   if (row >= n_rows) return;  // uniform per wave
@@ -160,8 +206,11 @@ __global__ __launch_bounds__(256) void select_kernel(const float* __restrict__ s
     if (lane == 0) cnt[row] = m;
     return;
   }
-  if (p.mode == kSelectThreshold) select_row_sized<NPL, false>(s, m, p.v[hp], 0, lane, out, cnt + row);
-  else select_row_sized<NPL, true>(s, m, 0.f, k, lane, out, cnt + row);
+  uint64_t* stage = stage_all[threadIdx.x >> 6];
+  if (p.mode == kSelectThreshold)
+    select_row_sized<NPL, false>(s, m, p.v[hp], 0, lane, out, cnt + row, stage);
+  else
+    select_row_sized<NPL, true>(s, m, 0.f, k, lane, out, cnt + row, stage);
 }
 
 template <int NPL>

@@ -149,6 +149,58 @@ def test_select_is_bit_exact_on_same_scores(NB, causal):
             assert np.array_equal(gi[r, :gc[r]], oi[r, :oc[r]]), (r, tau)
 
 
+def _structured_rows(kind, n, NB, rng):
+    """Score rows whose search interval either empties fast (a few large,
+    well separated masses over a tiny floor) or stays crowded (hundreds of
+    equal masses at the cut, or a dense uniform spread)."""
+    if kind == "separated":
+        r = np.full((n, NB), 1e-7)
+        for i in range(n):
+            top = rng.choice(NB, 24, replace=False)
+            r[i, top] = 0.6 ** np.arange(24) * rng.uniform(0.5, 1.0)
+    elif kind == "crowded_ties":
+        r = np.full((n, NB), 1e-7)
+        for i in range(n):
+            pick = rng.permutation(NB)
+            r[i, pick[:400]] = 0.002
+            r[i, pick[400:410]] = 0.02
+    else:  # uniform
+        r = rng.uniform(0.0, 1e-3, (n, NB))
+    return r.astype(np.float32)
+
+
+@pytest.mark.parametrize("kind", ["separated", "crowded_ties", "uniform"])
+def test_select_search_paths_bit_exact(kind):
+    """Rows of 1024 candidates, threshold and Top-K: the search either
+    finishes on the few values left in its interval or keeps scanning every
+    candidate; both must give the oracle's lists exactly."""
+    NB, H = 1024, 2
+    rng = np.random.default_rng({"separated": 11, "crowded_ties": 12, "uniform": 13}[kind])
+    full = _structured_rows(kind, H * NB, NB, rng).reshape(H, NB, NB)
+    dims = X.Dims(1, H, 1, NB * 128, 128, 0)
+    flat = full.reshape(H * NB, NB).astype(np.float64)
+    allb = np.tile(np.arange(NB, dtype=np.int32), H)
+    dev = torch.from_numpy(full).cuda()
+    for tau in (0.5, 0.9, 0.99):
+        print(f"select paths kind={kind} tau={tau}", flush=True)
+        idx, cnt = X.xattn_select(dev, dims, tau)
+        torch.cuda.synchronize()
+        oi, oc = oracle.select_rows(flat, allb, tau, False)
+        gi, gc = idx.cpu().numpy().reshape(H * NB, NB), cnt.cpu().numpy().reshape(-1)
+        assert np.array_equal(gc, oc)
+        for r in range(H * NB):
+            assert np.array_equal(gi[r, :gc[r]], oi[r, :oc[r]]), (r, tau)
+    for k in (1, 37, 500):
+        print(f"select paths kind={kind} topk={k}", flush=True)
+        idx, cnt = X.xattn_select_topk(dev, dims, k)
+        torch.cuda.synchronize()
+        oi, oc = oracle.select_topk_rows(flat, allb, np.int32(k), False)
+        gi, gc = idx.cpu().numpy().reshape(H * NB, NB), cnt.cpu().numpy().reshape(-1)
+        assert np.array_equal(gc, oc)
+        for r in range(H * NB):
+            assert np.array_equal(gi[r, :gc[r]], oi[r, :oc[r]]), (r, k)
+
+
 def test_select_on_oracle_scores_rounded_to_fp32():
     L, hq, hkv, S = 2048, 4, 2, 8
     x = _inputs(L, hq, hkv, seed=301)
