@@ -384,27 +384,53 @@ def main():
         dense_ms = e0.elapsed_time(e1) / a.dense_steps
         print(f"# dense mode {dense_ms:.2f} ms", file=sys.stderr, flush=True)
 
-    # dominant kernel of the step and its roofline (algorithmic FLOPs per launch)
+    # dominant kernel of the step and its roofline. Algorithmic work per launch:
+    # attention = computed blocks x 4*B^2*d FLOPs over their K/V (2*B*d bf16 =
+    # 64 KB per block, fetched per use) plus Q and O once; scoring = the reduced
+    # GEMM over Q and K read once plus its partial sums. The bound is the
+    # roof below the ridge point (peak FLOP/s / peak HBM B/s) at that
+    # arithmetic intensity.
     NR = w.seq // w.stride
     score_flops = 2.0 * NR * NR * w.stride * w.head_dim * dims.heads
     if w.causal:
         score_flops /= 2
+    q_bytes = dims.heads * w.seq * w.head_dim * 2.0
+    k_bytes = dims.batch * dims.hkv * w.seq * w.head_dim * 2.0
+    attn_bytes = computed_blocks * 2.0 * w.block * w.head_dim * 2 + 2 * q_bytes
+    score_bytes = q_bytes + k_bytes + dims.heads * NR * NB * 4.0 * (0.5 if w.causal else 1.0)
     kernels = {
-        "attn": {"ms": t_attn, "flops": attn_flops},
-        "score": {"ms": t_score, "flops": score_flops},
+        "attn": {"ms": t_attn, "flops": attn_flops, "bytes": attn_bytes},
+        "score": {"ms": t_score, "flops": score_flops, "bytes": score_bytes},
     }
     dom = max(kernels, key=lambda n: kernels[n]["ms"])
-    ach = kernels[dom]["flops"] / (kernels[dom]["ms"] * 1e-3) / 1e12
+    kd = kernels[dom]
+    ai = kd["flops"] / kd["bytes"]
+    ridge = PEAK_BF16_TFLOPS * 1e12 / (PEAK_HBM_GBS * 1e9)
+    tflops = kd["flops"] / (kd["ms"] * 1e-3) / 1e12
+    gbs = kd["bytes"] / (kd["ms"] * 1e-3) / 1e9
     traffic = read_traffic(a.traffic_file, w, dom)
     attn_traffic = read_traffic(a.traffic_file, w, "attn")
-    roofline = {"bound": "mfma", "kernel": dom, "achieved": round(ach, 2),
-                "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s", "frac": round(ach / PEAK_BF16_TFLOPS, 4),
-                "traffic": traffic,
-                "per_launch_flops": kernels[dom]["flops"],
-                "avg_launch_ms": round(kernels[dom]["ms"], 4),
-                "flops_convention": ("computed 128x128 blocks x 4*B^2*d (diagonal blocks in "
-                                     "full)" if dom == "attn" else
-                                     "2 * (L/S)^2 * S*d per head, halved when causal")}
+    if ai < ridge:
+        roofline = {"bound": "hbm", "kernel": dom, "achieved": round(gbs, 1),
+                    "peak": PEAK_HBM_GBS, "unit": "GB/s", "frac": round(gbs / PEAK_HBM_GBS, 4)}
+    else:
+        roofline = {"bound": "mfma", "kernel": dom, "achieved": round(tflops, 2),
+                    "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
+                    "frac": round(tflops / PEAK_BF16_TFLOPS, 4)}
+    roofline.update({
+        "traffic": traffic,
+        "per_launch_bytes": kd["bytes"],
+        "per_launch_flops": kd["flops"],
+        "avg_launch_ms": round(kd["ms"], 4),
+        "flop_per_byte": round(ai, 1), "ridge_flop_per_byte": round(ridge, 1),
+        "achieved_tflops": round(tflops, 2),
+        "attainable_tflops": round(min(PEAK_BF16_TFLOPS, ai * PEAK_HBM_GBS / 1e3), 1),
+        "convention": ("computed 128x128 blocks x 4*B^2*d FLOPs (diagonal blocks in full); "
+                       "bytes = 64 KB of K/V per computed block + Q + O; traffic = measured "
+                       "L2-boundary bytes, below the algorithmic bytes where K/V hit in L2"
+                       if dom == "attn" else
+                       "2 * (L/S)^2 * S*d FLOPs per head, halved when causal; bytes = Q + K "
+                       "+ partial sums")})
 
     cpu = None
     if not a.no_cpu_baseline:
