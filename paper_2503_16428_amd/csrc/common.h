@@ -30,14 +30,6 @@ __device__ __forceinline__ bf16x8 as_bf16x8(u32x4 v) { return __builtin_bit_cast
 
 __device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
 
-// Round-to-nearest-even fp32 -> bf16 pair packed in one dword (lo = a, hi = b).
-__device__ __forceinline__ uint32_t pack_bf16x2(float a, float b) {
-  uint32_t ua = __builtin_bit_cast(uint32_t, a), ub = __builtin_bit_cast(uint32_t, b);
-  ua = (ua + 0x7FFFu + ((ua >> 16) & 1u)) >> 16;
-  ub = (ub + 0x7FFFu + ((ub >> 16) & 1u)) & 0xFFFF0000u;
-  return ua | ub;
-}
-
 // Direct-to-LDS load of 16 bytes per lane: lane l's bytes land at LDS byte
 // address lds + 16 l (lds wave-uniform, passed through M0); the global address
 // is sbase (scalar) + voff (per lane, bytes). Issued as inline asm so the
@@ -68,15 +60,6 @@ __device__ __forceinline__ void barrier_nofence() {
 }
 
 #define XATTN_LDS_ADDR(p) ((uint32_t)(uintptr_t)((__attribute__((address_space(3))) void*)(p)))
-
-// Bijection blockIdx -> logical work index such that the workgroups one XCD
-// receives (blockIdx % 8 == x) cover one contiguous logical range; neighbours
-// in logical order then share that XCD's L2.
-__device__ __forceinline__ int xcd_remap(int bid, int n) {
-  const int x = bid % kNumXcd, k = bid / kNumXcd;
-  const int per = n / kNumXcd, rem = n % kNumXcd;
-  return x * per + (x < rem ? x : rem) + k;
-}
 
 }  // namespace xattn
 
