@@ -135,6 +135,37 @@ def read_traffic(path, w, kernel):
     return None
 
 
+def roofline_of(name, kd, traffic):
+    """Roofline record of one kernel from its algorithmic work per launch
+    (kd: ms, flops, bytes): the bound is the roof below the ridge point
+    (peak FLOP/s / peak HBM B/s) at the kernel's arithmetic intensity."""
+    ai = kd["flops"] / kd["bytes"]
+    ridge = PEAK_BF16_TFLOPS * 1e12 / (PEAK_HBM_GBS * 1e9)
+    tflops = kd["flops"] / (kd["ms"] * 1e-3) / 1e12
+    gbs = kd["bytes"] / (kd["ms"] * 1e-3) / 1e9
+    if ai < ridge:
+        r = {"bound": "hbm", "kernel": name, "achieved": round(gbs, 1),
+             "peak": PEAK_HBM_GBS, "unit": "GB/s", "frac": round(gbs / PEAK_HBM_GBS, 4)}
+    else:
+        r = {"bound": "mfma", "kernel": name, "achieved": round(tflops, 2),
+             "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s", "frac": round(tflops / PEAK_BF16_TFLOPS, 4)}
+    r.update({
+        "traffic": traffic,
+        "per_launch_bytes": kd["bytes"],
+        "per_launch_flops": kd["flops"],
+        "avg_launch_ms": round(kd["ms"], 4),
+        "flop_per_byte": round(ai, 1), "ridge_flop_per_byte": round(ridge, 1),
+        "achieved_tflops": round(tflops, 2),
+        "attainable_tflops": round(min(PEAK_BF16_TFLOPS, ai * PEAK_HBM_GBS / 1e3), 1),
+        "convention": ("computed 128x128 blocks x 4*B^2*d FLOPs (diagonal blocks in full); "
+                       "bytes = 64 KB of K/V per computed block + Q + O; traffic = measured "
+                       "L2-boundary bytes, below the algorithmic bytes where K/V hit in L2"
+                       if name == "attn" else
+                       "2 * (L/S)^2 * S*d FLOPs per head, halved when causal; bytes = Q + K "
+                       "+ partial sums")})
+    return r
+
+
 def sweep_main(a, w, q, k, v, dims, stream):
     """Every (tau, S) point of the sweep on the same inputs: K timed steps of
     score -> select -> sparse attention each, HIP events per stage."""
@@ -403,34 +434,9 @@ def main():
         "score": {"ms": t_score, "flops": score_flops, "bytes": score_bytes},
     }
     dom = max(kernels, key=lambda n: kernels[n]["ms"])
-    kd = kernels[dom]
-    ai = kd["flops"] / kd["bytes"]
-    ridge = PEAK_BF16_TFLOPS * 1e12 / (PEAK_HBM_GBS * 1e9)
-    tflops = kd["flops"] / (kd["ms"] * 1e-3) / 1e12
-    gbs = kd["bytes"] / (kd["ms"] * 1e-3) / 1e9
     traffic = read_traffic(a.traffic_file, w, dom)
     attn_traffic = read_traffic(a.traffic_file, w, "attn")
-    if ai < ridge:
-        roofline = {"bound": "hbm", "kernel": dom, "achieved": round(gbs, 1),
-                    "peak": PEAK_HBM_GBS, "unit": "GB/s", "frac": round(gbs / PEAK_HBM_GBS, 4)}
-    else:
-        roofline = {"bound": "mfma", "kernel": dom, "achieved": round(tflops, 2),
-                    "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
-                    "frac": round(tflops / PEAK_BF16_TFLOPS, 4)}
-    roofline.update({
-        "traffic": traffic,
-        "per_launch_bytes": kd["bytes"],
-        "per_launch_flops": kd["flops"],
-        "avg_launch_ms": round(kd["ms"], 4),
-        "flop_per_byte": round(ai, 1), "ridge_flop_per_byte": round(ridge, 1),
-        "achieved_tflops": round(tflops, 2),
-        "attainable_tflops": round(min(PEAK_BF16_TFLOPS, ai * PEAK_HBM_GBS / 1e3), 1),
-        "convention": ("computed 128x128 blocks x 4*B^2*d FLOPs (diagonal blocks in full); "
-                       "bytes = 64 KB of K/V per computed block + Q + O; traffic = measured "
-                       "L2-boundary bytes, below the algorithmic bytes where K/V hit in L2"
-                       if dom == "attn" else
-                       "2 * (L/S)^2 * S*d FLOPs per head, halved when causal; bytes = Q + K "
-                       "+ partial sums")})
+    roofline = roofline_of(dom, kernels[dom], traffic)
 
     cpu = None
     if not a.no_cpu_baseline:
