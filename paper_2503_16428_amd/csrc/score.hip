@@ -16,6 +16,8 @@
 // sum_{c in j} exp2(x - m). Kernel score_finalize
 // merges the tiles of each row (m_R = max_t m, l_R = sum_t l 2^(m - m_R)),
 // normalises, and averages the B/S reduced rows of each query block.
+#include <atomic>
+
 #include "common.h"
 
 using namespace xattn;
@@ -456,17 +458,20 @@ __global__ __launch_bounds__(256) void score_finalize(const float* __restrict__ 
 // Compute units of the current device, rounded down to a multiple of the 8
 // XCDs (cached per device).
 int persistent_workgroups() {
-  static int cached[64] = {};
+  static std::atomic<int> cached[64];  // static storage: starts at zero
   int dev = 0;
-  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) dev = 0;
-  if (cached[dev] == 0) {
+  if (hipGetDevice(&dev) != hipSuccess) dev = 0;
+  const bool cacheable = dev >= 0 && dev < 64;
+  int n = cacheable ? cached[dev].load(std::memory_order_relaxed) : 0;
+  if (n == 0) {
     int cus = 0;
     if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
         cus < kNumXcd)
-      cus = 256;
-    cached[dev] = cus / kNumXcd * kNumXcd;
+      cus = 256;  // any multiple of 8 is a valid grid; this only sizes it
+    n = cus / kNumXcd * kNumXcd;
+    if (cacheable) cached[dev].store(n, std::memory_order_relaxed);
   }
-  return cached[dev];
+  return n;
 }
 
 template <int NRB, bool CAUSAL>
