@@ -229,6 +229,34 @@ int xattn_threshold_dp(const double *perf, int heads, int max_adjust, int adjust
                        int32_t *adjust, double *best);
 
 /*
+ * The thresholds of the minimum-threshold prediction (Sec. 3.3): after a
+ * reductions of 10 % from tau0 a head's threshold is tau0 * 0.9^a, computed
+ * in fp64 and rounded once to the fp32 value the selection receives.
+ *   levels  host float [max_adjust + 1] (output): levels[a] for a = 0 .. max_adjust
+ * XATTN_ERR_ARG for a NULL array, tau0 <= 0 / not finite, or max_adjust < 0.
+ * Host only (no GPU).
+ */
+int xattn_threshold_levels(double tau0, int max_adjust, float *levels);
+
+/*
+ * The whole prediction step of Sec. 3.3 on a per-head error table: the
+ * dynamic program of xattn_threshold_dp with performance = minus the error
+ * (the assignment of exactly `adjustments` reductions with the least total
+ * error; on equal totals a head keeps fewer adjustments), followed by the
+ * thresholds it implies.
+ *   err        host double [heads][max_adjust + 1]: err[h][a] is head h's error
+ *              after a reductions (e.g. xattn_head_error_mean at levels[a]); finite
+ *   tau0       the threshold before any reduction (> 0)
+ *   adjust     host int32 [heads] (output), summing to `adjustments`
+ *   tau_h      host float [heads] (output): tau0 * 0.9^adjust[h] as in
+ *              xattn_threshold_levels, ready for xattn_select_heads
+ *   total_err  host double (output, may be NULL): the least total error
+ * Errors as xattn_threshold_dp, plus XATTN_ERR_ARG for a bad tau0. Host only.
+ */
+int xattn_threshold_predict(const double *err, int heads, int max_adjust, int adjustments,
+                            double tau0, int32_t *adjust, float *tau_h, double *total_err);
+
+/*
  * Per-head output error, the performance proxy for xattn_threshold_dp:
  * err[h] = sum (o - o_ref)^2 / sum o_ref^2 over head h's [L][D] outputs
  * (bf16 inputs, fp64 accumulation, a fixed order: deterministic).
@@ -239,6 +267,16 @@ int xattn_threshold_dp(const double *perf, int heads, int max_adjust, int adjust
 int xattn_head_error_workspace_size(const xattn_dims *dims, size_t *bytes);
 int xattn_head_error(const void *o, const void *o_ref, const xattn_dims *dims, double *err,
                      void *workspace, size_t workspace_bytes, void *stream);
+
+/*
+ * xattn_head_error averaged over the batch: err[h] for query head h < hq is
+ * (1 / batch) * sum_n of the error of row n * hq + h, added in batch order
+ * (the per-head table of the prediction covers heads of the model, not
+ * sequences). err is double [hq] device (output); the workspace is the one
+ * xattn_head_error_workspace_size() reports. Errors as xattn_head_error.
+ */
+int xattn_head_error_mean(const void *o, const void *o_ref, const xattn_dims *dims,
+                          double *err, void *workspace, size_t workspace_bytes, void *stream);
 
 /* Static description of a status code (never NULL). */
 const char *xattn_strerror(int status);

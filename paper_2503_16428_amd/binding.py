@@ -61,8 +61,9 @@ EXPORTS = [
     "xattn_select_topk", "xattn_select_ratio", "xattn_block_sparse_attn",
     "xattn_dense_attn", "xattn_forward_workspace_size", "xattn_forward_layout",
     "xattn_forward", "xattn_forward_scheduled", "xattn_threshold_dp",
-    "xattn_head_error_workspace_size", "xattn_head_error", "xattn_strerror", "xattn_last_error",
-    "xattn_version",
+    "xattn_threshold_levels", "xattn_threshold_predict",
+    "xattn_head_error_workspace_size", "xattn_head_error", "xattn_head_error_mean",
+    "xattn_strerror", "xattn_last_error", "xattn_version",
 ]
 
 
@@ -94,8 +95,11 @@ def lib() -> ctypes.CDLL:
         L.xattn_forward.argtypes = [P, P, P, PD, I, I, F, P, P, P, SZ, P]
         L.xattn_forward_scheduled.argtypes = [P, P, P, PD, I, I, F, I, I, P, P, P, SZ, P]
         L.xattn_threshold_dp.argtypes = [P, I, I, I, P, P]
+        L.xattn_threshold_levels.argtypes = [ctypes.c_double, I, P]
+        L.xattn_threshold_predict.argtypes = [P, I, I, I, ctypes.c_double, P, P, P]
         L.xattn_head_error_workspace_size.argtypes = [PD, PSZ]
         L.xattn_head_error.argtypes = [P, P, PD, P, P, SZ, P]
+        L.xattn_head_error_mean.argtypes = [P, P, PD, P, P, SZ, P]
         L.xattn_strerror.argtypes = [I]
         L.xattn_strerror.restype = ctypes.c_char_p
         L.xattn_last_error.restype = ctypes.c_char_p
@@ -117,13 +121,61 @@ def _check(status: int):
 def make_dims(q: torch.Tensor, k: torch.Tensor, causal: bool) -> Dims:
     if q.dim() == 3:
         batch, hq, seq, d = 1, q.shape[0], q.shape[1], q.shape[2]
-        hkv = k.shape[0]
+        hkv = k.shape[0] if k.dim() == 3 else -1
     elif q.dim() == 4:
         batch, hq, seq, d = q.shape
-        hkv = k.shape[1]
+        hkv = k.shape[1] if k.dim() == 4 else -1
     else:
         raise XAttnError(XATTN_ERR_ARG, f"q must be 3-D or 4-D, got {tuple(q.shape)}")
+    want_k = (hkv, seq, d) if q.dim() == 3 else (batch, hkv, seq, d)
+    if k.dim() != q.dim() or tuple(k.shape) != want_k:
+        raise XAttnError(XATTN_ERR_ARG, f"k must be [{'batch, ' if q.dim() == 4 else ''}hkv, "
+                                        f"seq, head_dim] matching q {tuple(q.shape)}, got "
+                                        f"{tuple(k.shape)}")
     return Dims(batch, hq, hkv, seq, d, 1 if causal else 0)
+
+
+def _check_shape(t, shape, dtype, name):
+    """Shape and dtype of a tensor the kernels read or write, checked before
+    the device check so that a mismatch never reaches a launch."""
+    if t is None:
+        return
+    if tuple(t.shape) != tuple(shape):
+        raise XAttnError(XATTN_ERR_ARG, f"{name} must have shape {tuple(shape)}, got "
+                                        f"{tuple(t.shape)}")
+    if t.dtype != dtype:
+        raise XAttnError(XATTN_ERR_ARG, f"{name} must be {dtype}, got {t.dtype}")
+
+
+def _qkv_dims(q, k, v, causal):
+    """Dims of an attention call: q, k, v bf16 with k.shape == v.shape."""
+    for t, n in ((q, "q"), (k, "k"), (v, "v")):
+        if t.dtype != torch.bfloat16:
+            raise XAttnError(XATTN_ERR_ARG, f"{n} must be torch.bfloat16, got {t.dtype}")
+    d = make_dims(q, k, causal)
+    if tuple(v.shape) != tuple(k.shape):
+        raise XAttnError(XATTN_ERR_ARG, f"v must have k's shape {tuple(k.shape)}, got "
+                                        f"{tuple(v.shape)}")
+    return d
+
+
+def _on_device(**tensors):
+    """Device and layout checks, after every shape check of the call."""
+    for n, t in tensors.items():
+        if t is not None:
+            _need(t, t.dtype, n)
+
+
+def _check_select_shapes(dims: Dims, block: int, scores=None, idx=None, cnt=None):
+    nb = dims.seq // block if block > 0 else 0
+    _check_shape(scores, (dims.heads, nb, nb), torch.float32, "scores")
+    _check_shape(idx, (dims.heads, nb, nb), torch.int32, "idx")
+    _check_shape(cnt, (dims.heads, nb), torch.int32, "cnt")
+
+
+def _check_outputs(q, dims: Dims, o=None, lse=None):
+    _check_shape(o, tuple(q.shape), torch.bfloat16, "o")
+    _check_shape(lse, (dims.heads, dims.seq), torch.float32, "lse")
 
 
 def _ptr(t):
@@ -164,19 +216,38 @@ def forward_layout(dims: Dims, block: int, stride: int) -> dict:
     return dict(zip(("scores", "idx", "cnt", "scratch"), (x.value for x in v)))
 
 
+def _qk_dims(q, k, causal):
+    for t, n in ((q, "q"), (k, "k")):
+        if t.dtype != torch.bfloat16:
+            raise XAttnError(XATTN_ERR_ARG, f"{n} must be torch.bfloat16, got {t.dtype}")
+    return make_dims(q, k, causal)
+
+
+def _check_workspace(workspace):
+    if workspace is not None and (workspace.dtype != torch.uint8 or workspace.dim() != 1):
+        raise XAttnError(XATTN_ERR_ARG, "workspace must be a 1-D torch.uint8 tensor")
+
+
+def _workspace(workspace, nbytes, device):
+    if workspace is None:
+        return torch.empty(max(nbytes, 1), dtype=torch.uint8, device=device)
+    _check_workspace(workspace)
+    _need(workspace, torch.uint8, "workspace")
+    return workspace
+
+
 def xattn_score(q, k, causal=True, block=BLOCK, stride=8, scores=None, workspace=None,
                 stream=None):
     """Antidiagonal block scores [batch*hq, NB, NB] (fp32)."""
-    _need(q, torch.bfloat16, "q")
-    _need(k, torch.bfloat16, "k")
-    d = make_dims(q, k, causal)
+    d = _qk_dims(q, k, causal)
+    _check_select_shapes(d, block, scores=scores)
+    _check_workspace(workspace)
+    _on_device(q=q, k=k, scores=scores, workspace=workspace)
     nb = d.seq // block if block > 0 else 0
     if scores is None:
         scores = torch.empty((d.heads, nb, nb), dtype=torch.float32, device=q.device)
     _need(scores, torch.float32, "scores")
-    if workspace is None:
-        workspace = torch.empty(score_workspace_size(d, block, stride), dtype=torch.uint8,
-                                device=q.device)
+    workspace = _workspace(workspace, score_workspace_size(d, block, stride), q.device)
     _check(lib().xattn_score(_ptr(q), _ptr(k), ctypes.byref(d), block, stride, _ptr(scores),
                              _ptr(workspace), workspace.numel(), _stream(stream)))
     return scores
@@ -186,24 +257,26 @@ def xattn_score_pattern(q, k, causal, block, stride, qsub, scores=None, workspac
                         stream=None):
     """Block scores with the sub-block positions (qsub[t], t): qsub a permutation of
     0..stride-1 (stride-1-t is the antidiagonal of xattn_score, t the diagonal)."""
-    _need(q, torch.bfloat16, "q")
-    _need(k, torch.bfloat16, "k")
-    d = make_dims(q, k, causal)
+    d = _qk_dims(q, k, causal)
+    _check_select_shapes(d, block, scores=scores)
+    qs = np.ascontiguousarray(qsub, dtype=np.int32)
+    if qs.shape != (stride,):
+        raise XAttnError(XATTN_ERR_ARG, f"qsub must hold {stride} entries, got {qs.shape}")
+    _check_workspace(workspace)
+    _on_device(q=q, k=k, scores=scores, workspace=workspace)
     nb = d.seq // block
     if scores is None:
         scores = torch.empty((d.heads, nb, nb), dtype=torch.float32, device=q.device)
-    if workspace is None:
-        workspace = torch.empty(score_workspace_size(d, block, stride), dtype=torch.uint8,
-                                device=q.device)
-    qs = np.ascontiguousarray(qsub, dtype=np.int32)
+    _need(scores, torch.float32, "scores")
+    workspace = _workspace(workspace, score_workspace_size(d, block, stride), q.device)
     _check(lib().xattn_score_pattern(_ptr(q), _ptr(k), ctypes.byref(d), block, stride,
                                      qs.ctypes.data_as(ctypes.c_void_p), _ptr(scores),
                                      _ptr(workspace), workspace.numel(), _stream(stream)))
     return scores
 
 
-def xattn_select(scores, dims: Dims, tau: float, block=BLOCK, idx=None, cnt=None, stream=None):
-    """find_blocks per row: (idx [H, NB, NB] int32, cnt [H, NB] int32)."""
+def _select_outputs(scores, dims, block, idx, cnt):
+    _check_select_shapes(dims, block, scores=scores, idx=idx, cnt=cnt)
     _need(scores, torch.float32, "scores")
     nb = dims.seq // block
     if idx is None:
@@ -212,20 +285,14 @@ def xattn_select(scores, dims: Dims, tau: float, block=BLOCK, idx=None, cnt=None
         cnt = torch.empty((dims.heads, nb), dtype=torch.int32, device=scores.device)
     _need(idx, torch.int32, "idx")
     _need(cnt, torch.int32, "cnt")
-    _check(lib().xattn_select(_ptr(scores), ctypes.byref(dims), block, float(tau), _ptr(idx),
-                              _ptr(cnt), _stream(stream)))
     return idx, cnt
 
 
-def _select_outputs(scores, dims, block, idx, cnt):
-    _need(scores, torch.float32, "scores")
-    nb = dims.seq // block
-    if idx is None:
-        idx = torch.full((dims.heads, nb, nb), -1, dtype=torch.int32, device=scores.device)
-    if cnt is None:
-        cnt = torch.empty((dims.heads, nb), dtype=torch.int32, device=scores.device)
-    _need(idx, torch.int32, "idx")
-    _need(cnt, torch.int32, "cnt")
+def xattn_select(scores, dims: Dims, tau: float, block=BLOCK, idx=None, cnt=None, stream=None):
+    """find_blocks per row: (idx [H, NB, NB] int32, cnt [H, NB] int32)."""
+    idx, cnt = _select_outputs(scores, dims, block, idx, cnt)
+    _check(lib().xattn_select(_ptr(scores), ctypes.byref(dims), block, float(tau), _ptr(idx),
+                              _ptr(cnt), _stream(stream)))
     return idx, cnt
 
 
@@ -264,18 +331,23 @@ def xattn_select_ratio(scores, dims: Dims, ratio_h, block=BLOCK, idx=None, cnt=N
     return idx, cnt
 
 
-def xattn_block_sparse_attn(q, k, v, idx, cnt, causal=True, block=BLOCK, o=None, lse=None,
-                            want_lse=True, stream=None):
-    """Attention over the listed key blocks: (o bf16 like q, lse fp32 [H, seq] or None)."""
-    for t, n in ((q, "q"), (k, "k"), (v, "v")):
-        _need(t, torch.bfloat16, n)
-    _need(idx, torch.int32, "idx")
-    _need(cnt, torch.int32, "cnt")
-    d = make_dims(q, k, causal)
+def _attn_outputs(q, d, o, lse, want_lse):
+    _check_outputs(q, d, o, lse)
     if o is None:
         o = torch.empty_like(q)
     if lse is None and want_lse:
         lse = torch.empty((d.heads, d.seq), dtype=torch.float32, device=q.device)
+    return o, lse
+
+
+def xattn_block_sparse_attn(q, k, v, idx, cnt, causal=True, block=BLOCK, o=None, lse=None,
+                            want_lse=True, stream=None):
+    """Attention over the listed key blocks: (o bf16 like q, lse fp32 [H, seq] or None)."""
+    d = _qkv_dims(q, k, v, causal)
+    _check_select_shapes(d, block, idx=idx, cnt=cnt)
+    _check_outputs(q, d, o, lse)
+    _on_device(q=q, k=k, v=v, idx=idx, cnt=cnt, o=o, lse=lse)
+    o, lse = _attn_outputs(q, d, o, lse, want_lse)
     _check(lib().xattn_block_sparse_attn(_ptr(q), _ptr(k), _ptr(v), ctypes.byref(d), block,
                                          _ptr(idx), _ptr(cnt), _ptr(o), _ptr(lse),
                                          _stream(stream)))
@@ -284,37 +356,19 @@ def xattn_block_sparse_attn(q, k, v, idx, cnt, causal=True, block=BLOCK, o=None,
 
 def xattn_dense_attn(q, k, v, causal=True, o=None, lse=None, want_lse=True, stream=None):
     """Dense (all candidate blocks) attention, same kernel as the sparse mode."""
-    for t, n in ((q, "q"), (k, "k"), (v, "v")):
-        _need(t, torch.bfloat16, n)
-    d = make_dims(q, k, causal)
-    if o is None:
-        o = torch.empty_like(q)
-    if lse is None and want_lse:
-        lse = torch.empty((d.heads, d.seq), dtype=torch.float32, device=q.device)
+    d = _qkv_dims(q, k, v, causal)
+    _check_outputs(q, d, o, lse)
+    _on_device(q=q, k=k, v=v, o=o, lse=lse)
+    o, lse = _attn_outputs(q, d, o, lse, want_lse)
     _check(lib().xattn_dense_attn(_ptr(q), _ptr(k), _ptr(v), ctypes.byref(d), _ptr(o),
                                   _ptr(lse), _stream(stream)))
     return o, lse
 
 
-def xattn_forward(q, k, v, causal=True, block=BLOCK, stride=8, tau=0.9, o=None, lse=None,
-                  workspace=None, want_lse=False, stream=None):
-    """score -> select -> sparse attention. Returns (o, lse, workspace views dict)."""
-    for t, n in ((q, "q"), (k, "k"), (v, "v")):
-        _need(t, torch.bfloat16, n)
-    d = make_dims(q, k, causal)
-    if workspace is None:
-        workspace = torch.empty(forward_workspace_size(d, block, stride), dtype=torch.uint8,
-                                device=q.device)
-    if o is None:
-        o = torch.empty_like(q)
-    if lse is None and want_lse:
-        lse = torch.empty((d.heads, d.seq), dtype=torch.float32, device=q.device)
-    _check(lib().xattn_forward(_ptr(q), _ptr(k), _ptr(v), ctypes.byref(d), block, stride,
-                               float(tau), _ptr(o), _ptr(lse), _ptr(workspace),
-                               workspace.numel(), _stream(stream)))
+def _forward_views(workspace, d, block, stride):
     lay = forward_layout(d, block, stride)
     nb = d.seq // block
-    views = {
+    return {
         "scores": workspace[lay["scores"]:lay["scores"] + d.heads * nb * nb * 4]
         .view(torch.float32).view(d.heads, nb, nb),
         "idx": workspace[lay["idx"]:lay["idx"] + d.heads * nb * nb * 4]
@@ -322,7 +376,21 @@ def xattn_forward(q, k, v, causal=True, block=BLOCK, stride=8, tau=0.9, o=None, 
         "cnt": workspace[lay["cnt"]:lay["cnt"] + d.heads * nb * 4]
         .view(torch.int32).view(d.heads, nb),
     }
-    return o, lse, views
+
+
+def xattn_forward(q, k, v, causal=True, block=BLOCK, stride=8, tau=0.9, o=None, lse=None,
+                  workspace=None, want_lse=False, stream=None):
+    """score -> select -> sparse attention. Returns (o, lse, workspace views dict)."""
+    d = _qkv_dims(q, k, v, causal)
+    _check_outputs(q, d, o, lse)
+    _check_workspace(workspace)
+    _on_device(q=q, k=k, v=v, o=o, lse=lse, workspace=workspace)
+    o, lse = _attn_outputs(q, d, o, lse, want_lse)
+    workspace = _workspace(workspace, forward_workspace_size(d, block, stride), q.device)
+    _check(lib().xattn_forward(_ptr(q), _ptr(k), _ptr(v), ctypes.byref(d), block, stride,
+                               float(tau), _ptr(o), _ptr(lse), _ptr(workspace),
+                               workspace.numel(), _stream(stream)))
+    return o, lse, _forward_views(workspace, d, block, stride)
 
 
 def xattn_forward_scheduled(q, k, v, step, warmup_steps=5, causal=False, block=BLOCK,
@@ -330,16 +398,13 @@ def xattn_forward_scheduled(q, k, v, step, warmup_steps=5, causal=False, block=B
                             want_lse=False, stream=None):
     """Dense attention for steps < warmup_steps, XAttention afterwards (video
     DiT schedule). Returns (o, lse); the workspace is allocated only when needed."""
-    for t, n in ((q, "q"), (k, "k"), (v, "v")):
-        _need(t, torch.bfloat16, n)
-    d = make_dims(q, k, causal)
-    if workspace is None and step >= warmup_steps:
-        workspace = torch.empty(forward_workspace_size(d, block, stride), dtype=torch.uint8,
-                                device=q.device)
-    if o is None:
-        o = torch.empty_like(q)
-    if lse is None and want_lse:
-        lse = torch.empty((d.heads, d.seq), dtype=torch.float32, device=q.device)
+    d = _qkv_dims(q, k, v, causal)
+    _check_outputs(q, d, o, lse)
+    _check_workspace(workspace)
+    _on_device(q=q, k=k, v=v, o=o, lse=lse, workspace=workspace)
+    o, lse = _attn_outputs(q, d, o, lse, want_lse)
+    if workspace is not None or step >= warmup_steps:
+        workspace = _workspace(workspace, forward_workspace_size(d, block, stride), q.device)
     _check(lib().xattn_forward_scheduled(_ptr(q), _ptr(k), _ptr(v), ctypes.byref(d), block,
                                          stride, float(tau), int(step), int(warmup_steps),
                                          _ptr(o), _ptr(lse), _ptr(workspace),
@@ -362,20 +427,65 @@ def threshold_dp(perf, adjustments: int):
     return adj, best.value
 
 
-def head_error(o, o_ref, causal=True, workspace=None, stream=None):
-    """Per-head relative squared error of o against o_ref (float64 [heads] on the device)."""
+def threshold_levels(tau0: float, max_adjust: int) -> np.ndarray:
+    """The thresholds after 0 .. max_adjust reductions of 10 % from tau0 (float32)."""
+    out = np.zeros(max(int(max_adjust), 0) + 1, dtype=np.float32)
+    _check(lib().xattn_threshold_levels(ctypes.c_double(tau0), int(max_adjust),
+                                        out.ctypes.data_as(ctypes.c_void_p)))
+    return out
+
+
+def threshold_predict(err, adjustments: int, tau0: float):
+    """Per-head thresholds from a per-head error table err [heads][max_adjust + 1]
+    (host): the assignment of exactly `adjustments` reductions with the least
+    total error. Returns (adjust int32 [heads], tau_h float32 [heads], total error)."""
+    e = np.ascontiguousarray(err, dtype=np.float64)
+    if e.ndim != 2 or e.shape[1] < 2:
+        raise XAttnError(XATTN_ERR_ARG, f"err must be [heads][max_adjust + 1], got {e.shape}")
+    adj = np.zeros(e.shape[0], dtype=np.int32)
+    tau_h = np.zeros(e.shape[0], dtype=np.float32)
+    best = ctypes.c_double(0.0)
+    _check(lib().xattn_threshold_predict(e.ctypes.data_as(ctypes.c_void_p), e.shape[0],
+                                         e.shape[1] - 1, int(adjustments), ctypes.c_double(tau0),
+                                         adj.ctypes.data_as(ctypes.c_void_p),
+                                         tau_h.ctypes.data_as(ctypes.c_void_p),
+                                         ctypes.byref(best)))
+    return adj, tau_h, best.value
+
+
+def _error_dims(o, o_ref, causal):
+    if o.dtype != torch.bfloat16 or o_ref.dtype != torch.bfloat16:
+        raise XAttnError(XATTN_ERR_ARG, "o and o_ref must be torch.bfloat16")
+    if tuple(o.shape) != tuple(o_ref.shape):
+        raise XAttnError(XATTN_ERR_ARG, f"o and o_ref must have the same shape, got "
+                                        f"{tuple(o.shape)} and {tuple(o_ref.shape)}")
+    d = make_dims(o, o, causal)
     _need(o, torch.bfloat16, "o")
     _need(o_ref, torch.bfloat16, "o_ref")
-    if o.shape != o_ref.shape:
-        raise XAttnError(XATTN_ERR_ARG, "o and o_ref must have the same shape")
-    d = make_dims(o, o if o.dim() == 3 else o, causal)
+    return d
+
+
+def head_error(o, o_ref, causal=True, workspace=None, stream=None):
+    """Per-head relative squared error of o against o_ref (float64 [heads] on the device)."""
+    d = _error_dims(o, o_ref, causal)
     n = ctypes.c_size_t(0)
     _check(lib().xattn_head_error_workspace_size(ctypes.byref(d), ctypes.byref(n)))
-    if workspace is None:
-        workspace = torch.empty(max(n.value, 1), dtype=torch.uint8, device=o.device)
+    workspace = _workspace(workspace, n.value, o.device)
     err = torch.empty(d.heads, dtype=torch.float64, device=o.device)
     _check(lib().xattn_head_error(_ptr(o), _ptr(o_ref), ctypes.byref(d), _ptr(err),
                                   _ptr(workspace), workspace.numel(), _stream(stream)))
+    return err
+
+
+def head_error_mean(o, o_ref, causal=True, workspace=None, stream=None):
+    """Per-query-head relative squared error averaged over the batch (float64 [hq])."""
+    d = _error_dims(o, o_ref, causal)
+    n = ctypes.c_size_t(0)
+    _check(lib().xattn_head_error_workspace_size(ctypes.byref(d), ctypes.byref(n)))
+    workspace = _workspace(workspace, n.value, o.device)
+    err = torch.empty(d.hq, dtype=torch.float64, device=o.device)
+    _check(lib().xattn_head_error_mean(_ptr(o), _ptr(o_ref), ctypes.byref(d), _ptr(err),
+                                       _ptr(workspace), workspace.numel(), _stream(stream)))
     return err
 
 

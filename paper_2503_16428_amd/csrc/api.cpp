@@ -337,8 +337,9 @@ int xattn_head_error_workspace_size(const xattn_dims* dims, size_t* bytes) {
   return ok();
 }
 
-int xattn_head_error(const void* o, const void* o_ref, const xattn_dims* dims, double* err,
-                     void* workspace, size_t workspace_bytes, void* stream) {
+static int head_error_common(const void* o, const void* o_ref, const xattn_dims* dims,
+                             double* err, void* workspace, size_t workspace_bytes,
+                             bool mean_over_batch, void* stream) {
   XattnShape s;
   int rc;
   if ((rc = check_dims(dims, &s))) return rc;
@@ -348,8 +349,19 @@ int xattn_head_error(const void* o, const void* o_ref, const xattn_dims* dims, d
   if (!workspace || workspace_bytes < need)
     return fail(XATTN_ERR_WORKSPACE, "workspace of %zu bytes needed, %zu given", need,
                 workspace ? workspace_bytes : (size_t)0);
-  return hip_status(launch_head_error(o, o_ref, s, err, workspace, (hipStream_t)stream),
+  return hip_status(launch_head_error(o, o_ref, s, err, workspace, mean_over_batch,
+                                      (hipStream_t)stream),
                     "xattn_head_error launch");
+}
+
+int xattn_head_error(const void* o, const void* o_ref, const xattn_dims* dims, double* err,
+                     void* workspace, size_t workspace_bytes, void* stream) {
+  return head_error_common(o, o_ref, dims, err, workspace, workspace_bytes, false, stream);
+}
+
+int xattn_head_error_mean(const void* o, const void* o_ref, const xattn_dims* dims,
+                          double* err, void* workspace, size_t workspace_bytes, void* stream) {
+  return head_error_common(o, o_ref, dims, err, workspace, workspace_bytes, true, stream);
 }
 
 const char* xattn_strerror(int status) {
@@ -365,6 +377,6 @@ const char* xattn_strerror(int status) {
 
 const char* xattn_last_error(void) { return g_err; }
 
-int xattn_version(void) { return 100; }
+int xattn_version(void) { return 10100; }
 
 }  // extern "C"

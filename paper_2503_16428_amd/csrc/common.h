@@ -95,7 +95,7 @@ hipError_t launch_select(const float* scores, const XattnShape& s, const SelectP
                          int32_t* idx, int32_t* cnt, hipStream_t st);
 size_t head_error_scratch_bytes(const XattnShape& s);
 hipError_t launch_head_error(const void* o, const void* o_ref, const XattnShape& s, double* err,
-                             void* scratch, hipStream_t st);
+                             void* scratch, bool mean_over_batch, hipStream_t st);
 hipError_t launch_attn(const void* q, const void* k, const void* v, const XattnShape& s,
                        const int32_t* idx, const int32_t* cnt, bool dense, void* o,
                        float* lse, hipStream_t st);

@@ -5,7 +5,9 @@
 // Pass 1: grid (chunk, head); each 256-thread workgroup streams one chunk of
 // a head with 16-byte loads, every thread sums in fp64, the workgroup reduces
 // in a fixed order and writes (num, den) for its chunk. Pass 2: one wave per
-// head adds its chunks in index order and divides. Deterministic.
+// head adds its chunks in index order and divides (for the batch mean, one
+// wave per query head then adds the batch's ratios in batch order and
+// divides by the batch). Deterministic.
 #include "common.h"
 
 using namespace xattn;
@@ -64,17 +66,33 @@ __global__ __launch_bounds__(kThreads) void head_error_partials(
   }
 }
 
-__global__ __launch_bounds__(64) void head_error_finish(const double2* __restrict__ part,
-                                                        int n_chunks, double* __restrict__ err) {
-  const int h = blockIdx.x;
-  if (threadIdx.x != 0) return;
+__device__ __forceinline__ double head_ratio(const double2* __restrict__ part, int n_chunks,
+                                             int h) {
   double tn = 0.0, td = 0.0;
   for (int c = 0; c < n_chunks; ++c) {
     const double2 v = part[(size_t)h * n_chunks + c];
     tn += v.x;
     td += v.y;
   }
-  err[h] = td > 0.0 ? tn / td : (tn > 0.0 ? INFINITY : 0.0);
+  return td > 0.0 ? tn / td : (tn > 0.0 ? INFINITY : 0.0);
+}
+
+// err[h] for every (batch, query head) row h; with mean_over_batch, err[h]
+// for h < hq is instead the mean of the batch's errors of query head h, added
+// in batch order.
+__global__ __launch_bounds__(64) void head_error_finish(const double2* __restrict__ part,
+                                                        int n_chunks, int batch, int hq,
+                                                        int mean_over_batch,
+                                                        double* __restrict__ err) {
+  const int h = blockIdx.x;
+  if (threadIdx.x != 0) return;
+  if (!mean_over_batch) {
+    err[h] = head_ratio(part, n_chunks, h);
+    return;
+  }
+  double sum = 0.0;
+  for (int n = 0; n < batch; ++n) sum += head_ratio(part, n_chunks, n * hq + h);
+  err[h] = sum / (double)batch;
 }
 
 }  // namespace
@@ -86,7 +104,7 @@ size_t head_error_scratch_bytes(const XattnShape& s) {
 }
 
 hipError_t launch_head_error(const void* o, const void* o_ref, const XattnShape& s, double* err,
-                             void* scratch, hipStream_t st) {
+                             void* scratch, bool mean_over_batch, hipStream_t st) {
   const long long per_head = (long long)s.seq * s.head_dim;
   const int n_chunks = (int)((per_head + kChunkElems - 1) / kChunkElems);
   hipLaunchKernelGGL(head_error_partials, dim3(n_chunks, s.HQ()), dim3(kThreads), 0, st,
@@ -94,7 +112,8 @@ hipError_t launch_head_error(const void* o, const void* o_ref, const XattnShape&
                      (double2*)scratch);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(head_error_finish, dim3(s.HQ()), dim3(64), 0, st, (const double2*)scratch,
-                     n_chunks, err);
+  hipLaunchKernelGGL(head_error_finish, dim3(mean_over_batch ? s.hq : s.HQ()), dim3(64), 0, st,
+                     (const double2*)scratch, n_chunks, s.batch, s.hq, mean_over_batch ? 1 : 0,
+                     err);
   return hipGetLastError();
 }

@@ -30,7 +30,7 @@ def test_library_exports_every_declared_symbol():
     L = ctypes.CDLL(X.lib_path())
     for name in declared_functions():
         assert hasattr(L, name), name
-    assert X.version() == 100
+    assert X.version() == 10100
 
 
 def test_nm_shows_exports():

@@ -31,6 +31,20 @@ def test_head_error_matches_oracle(H, L):
     np.testing.assert_allclose(got, want, rtol=1e-12, atol=0)
 
 
+def test_head_error_mean_over_batch_matches_oracle():
+    """Batch 3 x 4 query heads: err[h] = mean over the batch of the oracle's
+    per-(batch, head) errors."""
+    n, hq, L = 3, 4, 1024
+    a = W.random_bf16((n * hq, L, 128), seed=5, scale=1.0)
+    b = W.random_bf16((n * hq, L, 128), seed=6, scale=1.0)
+    got = X.head_error_mean(dev_bf16(a).view(n, hq, L, 128),
+                            dev_bf16(b).view(n, hq, L, 128)).cpu().numpy()
+    per = oracle.head_errors(W.bf16_bits_to_f32(a), W.bf16_bits_to_f32(b)).reshape(n, hq)
+    want = per.mean(axis=0)
+    print(f"batch mean: {got} vs {want}", flush=True)
+    np.testing.assert_allclose(got, want, rtol=1e-12, atol=0)
+
+
 @pytest.mark.parametrize("M,A", [(2, 1), (5, 2)])
 def test_predicted_thresholds_match_the_oracle_pipeline(M, A):
     w = W.small("dp", 2048, hq=4, hkv=2, stride=8, tau=0.9, seed=41)
@@ -49,6 +63,8 @@ def test_predicted_thresholds_match_the_oracle_pipeline(M, A):
         f = oracle.forward_rows(x["q"], x["k"], x["v"], w.block, w.stride, tau, True, rows=rows)
         err[:, a] = oracle.head_errors(f["o"].reshape(w.hq, w.seq, w.head_dim), o_d)
     adj_o, best_o = oracle.threshold_dp(-err, M)
+    np.testing.assert_array_equal(res["levels"],
+                                  oracle.thresholds_from_adjustments(0.9, range(A + 1)))
     print(f"  gpu err {res['err'].round(6).tolist()} adjust {res['adjust'].tolist()}")
     print(f"  oracle err {err.round(6).tolist()} adjust {adj_o}", flush=True)
     # the proxy tables agree to the output tolerance of bf16 attention
