@@ -5,18 +5,30 @@ One step = one full pass of the hot path over one layer of synthetic input:
 antidiagonal scoring -> threshold selection -> block-sparse attention, all
 heads. Default workload: 128K tokens, 32 query / 8 KV heads (GQA), head_dim
 128, causal, B = 128, S = 16, tau = 0.9, clustered Q/K with a local key bias.
+--workload picks another of the five synthetic layers (4K single head, 32K
+GQA, the 64K sweep, the 115,200-token video layer).
+
+Timing protocol: W untimed warm-up steps; then K steps, each preceded by a
+512 MB write that evicts the L2s and the Infinity Cache, each stage bracketed
+by HIP events on the launch stream; the per-step and per-stage figures are
+medians over the K steps. The K steps are bracketed by device synchronisation
+and their wall time (flushes included) is reported beside them.
 
 Prints ONE JSON line: ms per layer and dense-equivalent TFLOP/s (the value),
-per-stage times, density, speedup over the library's own dense mode, the
-roofline of the dominant kernel and the CPU oracle baseline on a sample.
+per-stage times, density, speedup over the library's own dense mode, the MFMA
+roofline of the dominant kernel with its measured traffic, the random-block
+gather rate of the attention's load pattern, the shader clock and software
+versions, and the CPU oracle baseline on a sample.
 """
 from __future__ import annotations
 
 import argparse
+import ctypes
+import hashlib
 import json
-import math
 import os
 import sys
+import threading
 import time
 
 ROOT = os.path.dirname(os.path.abspath(__file__))
@@ -27,17 +39,20 @@ import numpy as np  # noqa: E402
 
 import workloads as W  # noqa: E402
 
-PEAK_BF16_TFLOPS = 2500.0      # MI355X dense bf16 MFMA
-PEAK_HBM_GBS = 8000.0
+PEAK_BF16_TFLOPS = 2500.0      # MI355X dense bf16 MFMA (2.4 GHz)
+PEAK_HBM_GBS = 8000.0          # MI355X HBM3E
+FLUSH_BYTES = 512 << 20        # written before every timed step
+CSRC = os.path.join(ROOT, "paper_2503_16428_amd", "csrc")
+KERNEL_SOURCES = {"attn": ["attn.hip", "common.h"], "score": ["score.hip", "common.h"]}
 
 
-def parse():
+def parse(argv=None):
     ap = argparse.ArgumentParser(description=__doc__.splitlines()[0])
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--workload", default=None, choices=sorted(W.WORKLOADS),
-                    help="default c3 (c5 with --dit-schedule)")
+                    help="default c3 (c5 with --dit-schedule, c4 with --sweep)")
     ap.add_argument("--stride", type=int, default=None)
     ap.add_argument("--seq", type=int, default=None,
                     help="override the workload's sequence length (a multiple of 128, at "
@@ -64,14 +79,18 @@ def parse():
                          "(default 1); the step then selects with those thresholds")
     ap.add_argument("--sweep", action="store_true",
                     help="the 64K parameter sweep: tau in {0.8, 0.9, 0.95} x S in {4, 8, 16} "
-                         "plus tau = 1 (S = 8); per point the layer time, stage times and "
-                         "density; one JSON line with every point")
+                         "plus tau = 1 (S = 8); per point the layer time, stage times, density "
+                         "and MFMA rooflines; one JSON line with every point")
     ap.add_argument("--dit-schedule", default=None, metavar="T,W",
                     help="video-DiT denoising schedule: time T layer steps (step t uses "
                          "dense attention for t < W, XAttention afterwards); default "
                          "workload c5")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-dense", action="store_true")
+    ap.add_argument("--no-flush", action="store_true",
+                    help="skip the 512 MB cache-evicting write before each timed step")
+    ap.add_argument("--no-probe", action="store_true",
+                    help="skip the random 64 KB block gather probe")
     ap.add_argument("--dense-steps", type=int, default=3)
     ap.add_argument("--copy-calibration", action="store_true",
                     help="after the timed region, copy a 256 MiB buffer once (a plain copy "
@@ -80,13 +99,10 @@ def parse():
                     help="query-block rows the CPU oracle computes for the baseline")
     ap.add_argument("--traffic-file", default=os.path.join(ROOT, "profiles", "hbm_traffic.txt"),
                     help="HBM bytes per launch measured by rocprofv3 --pmc (if present)")
-    return ap.parse_args()
+    return ap.parse_args(argv)
 
 
-def dev_bf16(u16):
-    """uint16 bf16 bit patterns (host) -> torch bf16 device tensor."""
-    import torch
-    return torch.from_numpy(np.ascontiguousarray(u16).view(np.int16)).view(torch.bfloat16).cuda()
+# ---------------------------------------------------------------- host logic
 
 
 def dense_flops(w) -> float:
@@ -95,15 +111,266 @@ def dense_flops(w) -> float:
     return f / 2 if w.causal else f
 
 
+def score_flops(w) -> float:
+    """The reduced product of Algorithm 1: (L/S)^2 outputs of depth S*d per
+    head, 2 FLOPs per multiply-add, halved when causal."""
+    nr = w.seq // w.stride
+    f = 2.0 * nr * nr * w.stride * w.head_dim * w.hq * w.batch
+    return f / 2 if w.causal else f
+
+
+def attn_flops(computed_blocks: int, w) -> float:
+    """4 B^2 d per computed 128 x 128 block (QK^T and PV; diagonal blocks in full)."""
+    return computed_blocks * 4.0 * w.block * w.block * w.head_dim
+
+
+def source_hash(kernel: str, csrc: str = CSRC) -> str:
+    """Short hash of the sources a kernel is built from: a traffic figure is
+    only used while the kernel it was measured on is unchanged."""
+    h = hashlib.sha1()
+    for f in KERNEL_SOURCES[kernel]:
+        with open(os.path.join(csrc, f), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()[:12]
+
+
+def read_traffic(path, w, kernel, src_hash):
+    """Bytes per launch across the L2 boundary (rocprofv3 FETCH_SIZE +
+    WRITE_SIZE, calibrated against a copy kernel) from the profile summary:
+    lines 'workload kernel stride tau bytes source_hash'. None if absent, taken
+    for another configuration, or taken on another version of the kernel."""
+    if not os.path.exists(path):
+        return None
+    for line in open(path):
+        f = line.split()
+        if len(f) == 6 and not line.startswith("#") and f[0] == w.name and f[1] == kernel \
+                and int(f[2]) == w.stride and abs(float(f[3]) - w.tau) < 1e-9 \
+                and f[5] == src_hash:
+            return float(f[4])
+    return None
+
+
+def roofline_of(name, flops, ms, traffic):
+    """MFMA roofline record of one kernel: its algorithmic FLOPs per launch
+    (computed blocks x 4 B^2 d for the attention, the reduced product for the
+    scoring) over its event-timed launch duration, against the dense bf16
+    peak. Beside it, the measured bytes across the L2 boundary per launch
+    (rocprofv3 counters, when taken on this kernel version) as a rate and a
+    fraction of the HBM peak."""
+    tflops = flops / (ms * 1e-3) / 1e12
+    r = {"bound": "mfma", "kernel": name, "achieved": round(tflops, 2),
+         "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
+         "frac": round(tflops / PEAK_BF16_TFLOPS, 4),
+         "traffic": traffic, "per_launch_flops": flops, "avg_launch_ms": round(ms, 4)}
+    if traffic is not None:
+        gbs = traffic / (ms * 1e-3) / 1e9
+        r.update({"traffic_GBps": round(gbs, 1),
+                  "traffic_frac_of_hbm_peak": round(gbs / PEAK_HBM_GBS, 4)})
+    r["convention"] = (
+        "computed 128x128 blocks x 4*B^2*d FLOPs (diagonal blocks in full); traffic = "
+        "rocprofv3 FETCH_SIZE+WRITE_SIZE bytes per launch, copy-calibrated"
+        if name == "attn" else
+        "2*(L/S)^2*S*d FLOPs per head, halved when causal (xattn_score: partial-sum and "
+        "finalize launches); traffic = rocprofv3 FETCH_SIZE+WRITE_SIZE bytes per launch")
+    return r
+
+
+def median(xs):
+    return float(np.median(np.asarray(xs, dtype=np.float64)))
+
+
+def env_info():
+    """Software versions and host CPU of the run."""
+    info = {}
+    try:
+        info["rocm"] = open("/opt/rocm/.info/version").read().strip()
+    except OSError:
+        info["rocm"] = None
+    try:
+        import torch
+        info["torch"] = torch.__version__
+        info["torch_hip"] = torch.version.hip
+        info["device"] = torch.cuda.get_device_name(0) if torch.cuda.is_available() else None
+    except Exception as e:  # noqa: BLE001
+        info["torch"] = f"unavailable: {e}"
+    info.update(cpu_info())
+    return info
+
+
+def cpu_info():
+    model = None
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                model = line.split(":", 1)[1].strip()
+                break
+    except OSError:
+        pass
+    return {"cpu_model": model, "affinity_cpus": len(os.sched_getaffinity(0))}
+
+
+class ClockSampler:
+    """The GPU shader (GFX) clock read through amdsmi on a host thread every
+    few milliseconds while the timed region runs; reports the median in MHz
+    (None, with the reason, where amdsmi cannot read it)."""
+
+    def __init__(self, period_s=0.002):
+        self.period, self.samples, self.error = period_s, [], None
+        self._stop = threading.Event()
+        self._thr = None
+        try:
+            import amdsmi
+            amdsmi.amdsmi_init()
+            self._smi = amdsmi
+            self._h = amdsmi.amdsmi_get_processor_handles()[0]
+            self._read()
+        except Exception as e:  # noqa: BLE001
+            self.error = f"{type(e).__name__}: {e}"
+
+    def _read(self):
+        info = self._smi.amdsmi_get_clock_info(self._h, self._smi.AmdSmiClkType.GFX)
+        return float(info["clk"])
+
+    def _run(self):
+        while not self._stop.is_set():
+            try:
+                self.samples.append(self._read())
+            except Exception as e:  # noqa: BLE001
+                self.error = f"{type(e).__name__}: {e}"
+                return
+            time.sleep(self.period)
+
+    def start(self):
+        if self.error is None:
+            self._thr = threading.Thread(target=self._run, daemon=True)
+            self._thr.start()
+
+    def stop(self):
+        if self._thr is not None:
+            self._stop.set()
+            self._thr.join()
+        if self.error is None:
+            try:
+                self._smi.amdsmi_shut_down()
+            except Exception:  # noqa: BLE001
+                pass
+        return {"gfx_clock_mhz_median": median(self.samples) if self.samples else None,
+                "gfx_clock_samples": len(self.samples), "source": "amdsmi GFX clk",
+                "error": self.error}
+
+
+# ---------------------------------------------------------------- GPU legs
+
+
+def dev_bf16(u16):
+    """uint16 bf16 bit patterns (host) -> torch bf16 device tensor."""
+    import torch
+    return torch.from_numpy(np.ascontiguousarray(u16).view(np.int16)).view(torch.bfloat16).cuda()
+
+
+class Flusher:
+    """A 512 MB device buffer rewritten before each timed step, so no step
+    finds its inputs in the L2s or the 256 MB Infinity Cache."""
+
+    def __init__(self, enabled):
+        import torch
+        self.buf = torch.empty(FLUSH_BYTES // 4, dtype=torch.int32, device="cuda") \
+            if enabled else None
+        self.n = 0
+
+    def __call__(self):
+        if self.buf is not None:
+            self.n += 1
+            self.buf.fill_(self.n)
+
+
+def time_steps(stages, steps, warmup, stream, flush):
+    """Run warmup untimed steps, then `steps` timed ones (flush before each,
+    HIP events around each stage on the launch stream). Returns (per-stage
+    event times [steps][n_stages] in ms, wall seconds of the timed steps)."""
+    import torch
+    for _ in range(warmup):
+        for f in stages:
+            f()
+    torch.cuda.synchronize()
+    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(len(stages) + 1)]
+           for _ in range(steps)]
+    t0 = time.perf_counter()
+    for i in range(steps):
+        flush()
+        evs[i][0].record(stream)
+        for j, f in enumerate(stages):
+            f()
+            evs[i][j + 1].record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    st = np.array([[e[j].elapsed_time(e[j + 1]) for j in range(len(stages))] for e in evs])
+    return st, wall
+
+
+def gather_probe(stream, per_wg=64, n_wg=4096, seed=7):
+    """Rate of the attention kernel's K/V load pattern alone (tracked probe
+    kernel, libxattn_probe.so): workgroups stream random 64 KB blocks into LDS
+    with the kernel's direct-to-LDS loads. Buffers of 64 MB (one KV group's
+    K+V at 128K tokens: Infinity-Cache resident) and 2 GB (HBM)."""
+    import torch
+    from paper_2503_16428_amd import build as B
+    if not os.path.exists(B.PROBE_LIB):
+        return {"error": "libxattn_probe.so not built"}
+    lib = ctypes.CDLL(B.PROBE_LIB)
+    lib.xattn_probe_gather.argtypes = [ctypes.c_void_p, ctypes.c_int, ctypes.c_void_p,
+                                       ctypes.c_int, ctypes.c_int, ctypes.c_void_p,
+                                       ctypes.c_void_p]
+    g = torch.Generator(device="cuda").manual_seed(seed)
+    sink = torch.empty(n_wg, dtype=torch.int32, device="cuda")
+    out = {"kernel": "gather_probe_kernel", "blocks_per_launch": per_wg * n_wg,
+           "bytes_per_launch": per_wg * n_wg * 65536}
+    for label, mb in (("infinity_cache_64MB", 64), ("hbm_2GB", 2048)):
+        nblk = mb * 16
+        buf = torch.ones(nblk * 32768, dtype=torch.bfloat16, device="cuda")
+        blocks = torch.randint(0, nblk, (n_wg * per_wg,), generator=g, device="cuda",
+                               dtype=torch.int32)
+
+        def launch():
+            rc = lib.xattn_probe_gather(ctypes.c_void_p(buf.data_ptr()), nblk,
+                                        ctypes.c_void_p(blocks.data_ptr()), per_wg, n_wg,
+                                        ctypes.c_void_p(sink.data_ptr()),
+                                        ctypes.c_void_p(stream.cuda_stream))
+            if rc != 0:
+                raise RuntimeError(f"gather probe launch failed ({rc})")
+
+        launch()
+        torch.cuda.synchronize()
+        ts = []
+        for _ in range(5):
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record(stream)
+            launch()
+            e1.record(stream)
+            torch.cuda.synchronize()
+            ts.append(e0.elapsed_time(e1))
+        ms = median(ts)
+        out[label] = {"ms": round(ms, 4),
+                      "TBps": round(out["bytes_per_launch"] / (ms * 1e-3) / 1e12, 3)}
+        del buf, blocks
+    return out
+
+
 def cpu_baseline(w, x, n_rows: int):
     """The CPU oracle (fp64, OpenMP) on a bounded sample of query-block rows:
     score + select + sparse attention for those rows, reported as dense-
     equivalent TFLOP/s of the rows it processed."""
     import oracle
     NB = w.n_blocks
+    H = w.hq * w.batch
+    total = H * NB
     rng = np.random.default_rng(12345)
-    heads = rng.integers(0, w.hq * w.batch, n_rows).astype(np.int32)
-    blocks = np.linspace(0, NB - 1, n_rows).round().astype(np.int32)
+    if n_rows >= total:
+        heads, blocks = oracle.all_rows(H, NB)
+    else:
+        pick = np.sort(rng.choice(total, n_rows, replace=False))
+        heads, blocks = (pick // NB).astype(np.int32), (pick % NB).astype(np.int32)
+    n_rows = len(heads)
     t0 = time.perf_counter()
     f = oracle.forward_rows(x["q"], x["k"], x["v"], w.block, w.stride, w.tau, w.causal,
                             rows=(heads, blocks))
@@ -112,63 +379,34 @@ def cpu_baseline(w, x, n_rows: int):
     flops = float((4.0 * w.block * w.block * w.head_dim * kv).sum())
     if w.causal:
         flops -= 4.0 * w.block * w.block * w.head_dim * n_rows / 2   # half diagonal
+    ci = cpu_info()
     return {
         "value": flops / dt / 1e12, "unit": "TFLOP/s (dense-equivalent)",
         "cores": oracle.num_threads(), "kind": "oracle",
-        "sample": f"{n_rows} query-block rows (random heads, blocks spread over 0..{NB - 1}) "
-                  f"of the same layer: score+select+sparse attention in fp64, {dt:.1f} s",
+        "sample": f"{n_rows} of {total} query-block rows (distinct, seeded) of the same "
+                  f"layer: score+select+sparse attention in fp64, {dt:.1f} s",
         "seconds": dt, "rows_density": float(f["cnt"].sum() / kv.sum()),
+        "cpu_model": ci["cpu_model"], "affinity_cpus": ci["affinity_cpus"],
+        "threads": oracle.num_threads(),
     }
 
 
-def read_traffic(path, w, kernel):
-    """HBM bytes per launch (FETCH_SIZE + WRITE_SIZE, calibrated against a copy
-    kernel) from the profile summary: lines 'workload kernel stride tau bytes'.
-    None if absent or taken for another configuration."""
-    if not os.path.exists(path):
-        return None
-    for line in open(path):
-        f = line.split()
-        if len(f) == 5 and not line.startswith("#") and f[0] == w.name and f[1] == kernel \
-                and int(f[2]) == w.stride and abs(float(f[3]) - w.tau) < 1e-9:
-            return float(f[4])
-    return None
+def density_of(c, w, heads):
+    NB = w.n_blocks
+    cand = (np.arange(1, NB + 1) if w.causal else np.full(NB, NB)).sum() * heads
+    return float(c.sum() / cand)
 
 
-def roofline_of(name, kd, traffic):
-    """Roofline record of one kernel from its algorithmic work per launch
-    (kd: ms, flops, bytes): the bound is the roof below the ridge point
-    (peak FLOP/s / peak HBM B/s) at the kernel's arithmetic intensity."""
-    ai = kd["flops"] / kd["bytes"]
-    ridge = PEAK_BF16_TFLOPS * 1e12 / (PEAK_HBM_GBS * 1e9)
-    tflops = kd["flops"] / (kd["ms"] * 1e-3) / 1e12
-    gbs = kd["bytes"] / (kd["ms"] * 1e-3) / 1e9
-    if ai < ridge:
-        r = {"bound": "hbm", "kernel": name, "achieved": round(gbs, 1),
-             "peak": PEAK_HBM_GBS, "unit": "GB/s", "frac": round(gbs / PEAK_HBM_GBS, 4)}
-    else:
-        r = {"bound": "mfma", "kernel": name, "achieved": round(tflops, 2),
-             "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s", "frac": round(tflops / PEAK_BF16_TFLOPS, 4)}
-    r.update({
-        "traffic": traffic,
-        "per_launch_bytes": kd["bytes"],
-        "per_launch_flops": kd["flops"],
-        "avg_launch_ms": round(kd["ms"], 4),
-        "flop_per_byte": round(ai, 1), "ridge_flop_per_byte": round(ridge, 1),
-        "achieved_tflops": round(tflops, 2),
-        "attainable_tflops": round(min(PEAK_BF16_TFLOPS, ai * PEAK_HBM_GBS / 1e3), 1),
-        "convention": ("computed 128x128 blocks x 4*B^2*d FLOPs (diagonal blocks in full); "
-                       "bytes = 64 KB of K/V per computed block + Q + O; traffic = measured "
-                       "L2-boundary bytes, below the algorithmic bytes where K/V hit in L2"
-                       if name == "attn" else
-                       "2 * (L/S)^2 * S*d FLOPs per head, halved when causal; bytes = Q + K "
-                       "+ partial sums")})
-    return r
+def metric_name(w):
+    if w.name.startswith("c3_128k") and w.seq == 131072:
+        return "ms/layer + dense-equiv TFLOP/s of scored block-sparse prefill at 128K"
+    return f"ms/layer + dense-equiv TFLOP/s of scored block-sparse prefill at {w.seq} tokens"
 
 
-def sweep_main(a, w, q, k, v, dims, stream):
-    """Every (tau, S) point of the sweep on the same inputs: K timed steps of
-    score -> select -> sparse attention each, HIP events per stage."""
+def sweep_main(a, w, q, k, v, dims, stream, flush, x):
+    """Every (tau, S) point of the sweep on the same inputs: the protocol's K
+    timed steps of score -> select -> sparse attention per point, MFMA
+    rooflines of both GEMM-shaped kernels per point."""
     import torch
     import paper_2503_16428_amd as X
     NB = w.n_blocks
@@ -178,53 +416,54 @@ def sweep_main(a, w, q, k, v, dims, stream):
     o = torch.empty_like(q)
     points = []
     dflops = dense_flops(w)
+    clock = ClockSampler()
+    clock.start()
     for tau, S in W.C4_SWEEP:
+        wp = w.with_(tau=tau, stride=S)
         ws = torch.empty(X.score_workspace_size(dims, w.block, S), dtype=torch.uint8,
                          device=q.device)
-
-        def step(ev=None):
-            if ev is not None:
-                ev[0].record(stream)
-            X.xattn_score(q, k, w.causal, w.block, S, scores=scores, workspace=ws)
-            if ev is not None:
-                ev[1].record(stream)
-            X.xattn_select(scores, dims, tau, w.block, idx=idx, cnt=cnt)
-            if ev is not None:
-                ev[2].record(stream)
-            X.xattn_block_sparse_attn(q, k, v, idx, cnt, w.causal, w.block, o=o,
-                                      want_lse=False)
-            if ev is not None:
-                ev[3].record(stream)
-
-        for _ in range(a.warmup):
-            step()
-        torch.cuda.synchronize()
-        evs = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(a.steps)]
-        t0 = time.perf_counter()
-        for i in range(a.steps):
-            step(evs[i])
-        torch.cuda.synchronize()
-        ms = (time.perf_counter() - t0) * 1e3 / a.steps
-        st = np.array([[e[0].elapsed_time(e[1]), e[1].elapsed_time(e[2]),
-                        e[2].elapsed_time(e[3])] for e in evs]).mean(0)
+        stages = [
+            lambda: X.xattn_score(q, k, w.causal, w.block, S, scores=scores, workspace=ws),
+            lambda: X.xattn_select(scores, dims, tau, w.block, idx=idx, cnt=cnt),
+            lambda: X.xattn_block_sparse_attn(q, k, v, idx, cnt, w.causal, w.block, o=o,
+                                              want_lse=False),
+        ]
+        st, wall = time_steps(stages, a.steps, a.warmup, stream, flush)
+        t_score, t_select, t_attn = (median(st[:, j]) for j in range(3))
+        ms = median(st.sum(1))
         c = cnt.cpu().numpy().astype(np.int64)
-        dens = float(c.sum() / ((np.arange(1, NB + 1) if w.causal else np.full(NB, NB)).sum()
-                               * dims.heads))
-        points.append({"tau": tau, "stride": S, "ms_per_step": round(ms, 4),
-                       "stages_ms": {"score": round(float(st[0]), 4),
-                                     "select": round(float(st[1]), 4),
-                                     "attn": round(float(st[2]), 4)},
-                       "density": round(dens, 5),
-                       "dense_equiv_tflops": round(dflops / (ms * 1e-3) / 1e12, 1)})
+        blocks = int(c.sum())
+        dens = density_of(c, w, dims.heads)
+        tr_a = read_traffic(a.traffic_file, wp, "attn", source_hash("attn"))
+        tr_s = read_traffic(a.traffic_file, wp, "score", source_hash("score"))
+        points.append({
+            "tau": tau, "stride": S, "ms_per_step": round(ms, 4),
+            "stages_ms": {"score": round(t_score, 4), "select": round(t_select, 4),
+                          "attn": round(t_attn, 4)},
+            "density": round(dens, 5),
+            "dense_equiv_tflops": round(dflops / (ms * 1e-3) / 1e12, 1),
+            "score_select_share": round((t_score + t_select) / (t_score + t_select + t_attn), 4),
+            "roofline_attn": roofline_of("attn", attn_flops(blocks, w), t_attn, tr_a),
+            "roofline_score": roofline_of("score", score_flops(wp), t_score, tr_s)})
         print(f"# tau={tau} S={S}: {ms:.3f} ms, density {dens:.4f}", file=sys.stderr, flush=True)
+    clk = clock.stop()
     ref = next(p for p in points if p["tau"] == 0.9 and p["stride"] == w.stride)
+    dom = "attn" if ref["stages_ms"]["attn"] >= ref["stages_ms"]["score"] else "score"
+    cpu = None
+    if not a.no_cpu_baseline:
+        print("# cpu baseline (oracle) ...", file=sys.stderr, flush=True)
+        cpu = cpu_baseline(w, x, a.cpu_rows)
+        cpu["seconds"] = round(cpu["seconds"], 2)
+        cpu["value"] = round(cpu["value"], 6)
     out = {
         "metric": "ms/layer + dense-equiv TFLOP/s of scored block-sparse prefill, 64K sweep",
         "value": ref["dense_equiv_tflops"], "unit": "TFLOP/s (dense-equivalent)",
         "n_gpus": 1, "steps": a.steps, "warmup": a.warmup, "ms_per_step": ref["ms_per_step"],
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "bf16",
-        "data": "synthetic", "config": dict(w.describe(), sweep="tau x S; value at tau=0.9, S=8"),
-        "sweep": points, "roofline": None, "cpu_baseline": None,
+        "data": "synthetic",
+        "config": dict(w.describe(), sweep="tau x S; value at tau=0.9, S=8"),
+        "protocol": protocol_note(a), "clock": clk, "env": env_info(),
+        "sweep": points, "roofline": ref[f"roofline_{dom}"], "cpu_baseline": cpu,
     }
     print(json.dumps(out), flush=True)
 
@@ -259,8 +498,8 @@ def schedule_main(a, w, q, k, v, dims, stream):
     per = np.array([e[0].elapsed_time(e[1]) for e in evs])
     is_dense = np.array([(i % T) < Wm for i in range(a.steps)])
     ms_step = wall * 1e3 / a.steps
-    dense_ms = float(per[is_dense].mean()) if is_dense.any() else None
-    sparse_ms = float(per[~is_dense].mean()) if (~is_dense).any() else None
+    dense_ms = float(np.median(per[is_dense])) if is_dense.any() else None
+    sparse_ms = float(np.median(per[~is_dense])) if (~is_dense).any() else None
     value = dense_flops(w) / (ms_step * 1e-3) / 1e12
     out = {
         "metric": "ms per denoising-step layer + dense-equiv TFLOP/s under the video-DiT "
@@ -274,13 +513,19 @@ def schedule_main(a, w, q, k, v, dims, stream):
         "xattn_step_ms": None if sparse_ms is None else round(sparse_ms, 4),
         "speedup_vs_all_dense": (None if dense_ms is None else
                                  round(dense_ms / float(per.mean()), 3)),
-        "roofline": None, "cpu_baseline": None,
+        "env": env_info(), "roofline": None, "cpu_baseline": None,
     }
     print(json.dumps(out), flush=True)
 
 
-def main():
-    a = parse()
+def protocol_note(a):
+    return (f"{a.warmup} untimed warm-up steps; {a.steps} timed steps, each after a "
+            f"{'512 MB cache-evicting write' if not a.no_flush else 'no flush'}; HIP events "
+            f"per stage on the launch stream; medians over the timed steps")
+
+
+def main(argv=None):
+    a = parse(argv)
     if a.gpus != 1:
         print(json.dumps({"error": "this benchmark runs on exactly one GPU; multi-GPU runs are "
                                    "not part of it (--gpus must be 1)"}), flush=True)
@@ -298,24 +543,25 @@ def main():
     NB = w.n_blocks
     t0 = time.perf_counter()
     x = W.generate(w, threads=16)
-    gen_s = time.perf_counter() - t0
-    print(f"# generated {w.name} in {gen_s:.1f} s", file=sys.stderr, flush=True)
+    print(f"# generated {w.name} in {time.perf_counter() - t0:.1f} s", file=sys.stderr,
+          flush=True)
     q, k, v = (dev_bf16(x[n]) for n in "qkv")
     dev = q.device
     dims = X.make_dims(q, k, w.causal)
+    stream = torch.cuda.current_stream()
+    flush = Flusher(not a.no_flush)
+    if a.dit_schedule:
+        schedule_main(a, w, q, k, v, dims, stream)
+        return
+    if a.sweep:
+        sweep_main(a, w, q, k, v, dims, stream, flush, x)
+        return
     scores = torch.empty((dims.heads, NB, NB), dtype=torch.float32, device=dev)
     idx = torch.empty((dims.heads, NB, NB), dtype=torch.int32, device=dev)
     cnt = torch.empty((dims.heads, NB), dtype=torch.int32, device=dev)
     o = torch.empty_like(q)
     ws = torch.empty(X.score_workspace_size(dims, w.block, w.stride), dtype=torch.uint8,
                      device=dev)
-    stream = torch.cuda.current_stream()
-    if a.dit_schedule:
-        schedule_main(a, w, q, k, v, dims, stream)
-        return
-    if a.sweep:
-        sweep_main(a, w, q, k, v, dims, stream)
-        return
     lo_hi = [float(t) for t in a.tau_heads.split(",")]
     tau_h = np.linspace(lo_hi[0], lo_hi[-1], w.hq).astype(np.float32)
     prediction = None
@@ -357,40 +603,22 @@ def main():
             X.xattn_score_pattern(q, k, w.causal, w.block, w.stride, qsub, scores=scores,
                                   workspace=ws)
 
-    def step(ev=None):
-        if ev is not None:
-            ev[0].record(stream)
-        score()
-        if ev is not None:
-            ev[1].record(stream)
-        select()
-        if ev is not None:
-            ev[2].record(stream)
+    def attend():
         X.xattn_block_sparse_attn(q, k, v, idx, cnt, w.causal, w.block, o=o, want_lse=False)
-        if ev is not None:
-            ev[3].record(stream)
 
-    for _ in range(a.warmup):
-        step()
-    torch.cuda.synchronize()
-    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(a.steps)]
-    torch.cuda.synchronize()
-    t0 = time.perf_counter()
-    for i in range(a.steps):
-        step(evs[i])
-    torch.cuda.synchronize()
-    wall = time.perf_counter() - t0
+    clock = ClockSampler()
+    clock.start()
+    st, wall = time_steps([score, select, attend], a.steps, a.warmup, stream, flush)
+    clk = clock.stop()
     print(f"# timed {a.steps} steps in {wall:.2f} s", file=sys.stderr, flush=True)
-    st = np.array([[e[0].elapsed_time(e[1]), e[1].elapsed_time(e[2]), e[2].elapsed_time(e[3])]
-                   for e in evs])
-    ms_step = wall * 1e3 / a.steps
-    t_score, t_select, t_attn = (float(v) for v in st.mean(0))
+    t_score, t_select, t_attn = (median(st[:, j]) for j in range(3))
+    ms_step = median(st.sum(1))
 
     c = cnt.cpu().numpy().astype(np.int64)
-    cand = (np.arange(1, NB + 1) if w.causal else np.full(NB, NB)) * dims.heads
-    density = float(c.sum() / cand.sum())
+    density = density_of(c, w, dims.heads)
     computed_blocks = int(c.sum())
-    attn_flops = computed_blocks * 4.0 * w.block * w.block * w.head_dim
+    a_flops = attn_flops(computed_blocks, w)
+    s_flops = score_flops(w)
     dflops = dense_flops(w)
     stage_sum = t_score + t_select + t_attn
 
@@ -404,52 +632,36 @@ def main():
 
     dense_ms = None
     if not a.no_dense:
-        X.xattn_dense_attn(q, k, v, w.causal, o=o, want_lse=False)
-        torch.cuda.synchronize()
-        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-        e0.record(stream)
-        for _ in range(a.dense_steps):
-            X.xattn_dense_attn(q, k, v, w.causal, o=o, want_lse=False)
-        e1.record(stream)
-        torch.cuda.synchronize()
-        dense_ms = e0.elapsed_time(e1) / a.dense_steps
+        dense = [lambda: X.xattn_dense_attn(q, k, v, w.causal, o=o, want_lse=False)]
+        dst_, _ = time_steps(dense, a.dense_steps, 1, stream, flush)
+        dense_ms = median(dst_[:, 0])
         print(f"# dense mode {dense_ms:.2f} ms", file=sys.stderr, flush=True)
 
-    # dominant kernel of the step and its roofline. Algorithmic work per launch:
-    # attention = computed blocks x 4*B^2*d FLOPs over their K/V (2*B*d bf16 =
-    # 64 KB per block, fetched per use) plus Q and O once; scoring = the reduced
-    # GEMM over Q and K read once plus its partial sums. The bound is the
-    # roof below the ridge point (peak FLOP/s / peak HBM B/s) at that
-    # arithmetic intensity.
-    NR = w.seq // w.stride
-    score_flops = 2.0 * NR * NR * w.stride * w.head_dim * dims.heads
-    if w.causal:
-        score_flops /= 2
-    q_bytes = dims.heads * w.seq * w.head_dim * 2.0
-    k_bytes = dims.batch * dims.hkv * w.seq * w.head_dim * 2.0
-    attn_bytes = computed_blocks * 2.0 * w.block * w.head_dim * 2 + 2 * q_bytes
-    score_bytes = q_bytes + k_bytes + dims.heads * NR * NB * 4.0 * (0.5 if w.causal else 1.0)
-    kernels = {
-        "attn": {"ms": t_attn, "flops": attn_flops, "bytes": attn_bytes},
-        "score": {"ms": t_score, "flops": score_flops, "bytes": score_bytes},
-    }
-    dom = max(kernels, key=lambda n: kernels[n]["ms"])
-    traffic = read_traffic(a.traffic_file, w, dom)
-    attn_traffic = read_traffic(a.traffic_file, w, "attn")
-    roofline = roofline_of(dom, kernels[dom], traffic)
+    probe = None
+    if not a.no_probe:
+        probe = gather_probe(stream)
+
+    # dominant kernel of the step and its MFMA roofline (both GEMM-shaped
+    # kernels are priced against the bf16 peak; the measured traffic sits
+    # beside the attention's)
+    kernels = {"attn": (a_flops, t_attn), "score": (s_flops, t_score)}
+    dom = max(kernels, key=lambda n: kernels[n][1])
+    traffic = read_traffic(a.traffic_file, w, dom, source_hash(dom))
+    roofline = roofline_of(dom, kernels[dom][0], kernels[dom][1], traffic)
+    other = "score" if dom == "attn" else "attn"
+    other_traffic = read_traffic(a.traffic_file, w, other, source_hash(other))
 
     cpu = None
     if not a.no_cpu_baseline:
         print("# cpu baseline (oracle) ...", file=sys.stderr, flush=True)
         cpu = cpu_baseline(w, x, a.cpu_rows)
         cpu["seconds"] = round(cpu["seconds"], 2)
-        # the sample's rate extrapolated to the whole layer (same unit as value)
         cpu["extrapolated_s_per_layer"] = round(dflops / (cpu["value"] * 1e12), 2)
         cpu["value"] = round(cpu["value"], 6)
 
     value = dflops / (ms_step * 1e-3) / 1e12
     out = {
-        "metric": "ms/layer + dense-equiv TFLOP/s of scored block-sparse prefill at 128K",
+        "metric": metric_name(w),
         "value": round(value, 3),
         "unit": "TFLOP/s (dense-equivalent)",
         "n_gpus": 1, "steps": a.steps, "warmup": a.warmup,
@@ -465,19 +677,25 @@ def main():
             "select": {"heads": {"tau_h": [round(float(t), 4) for t in tau_h]},
                        "topk": {"k_blocks": a.topk},
                        "ratio": {"ratio": a.ratio}}[a.select_mode] | {"mode": a.select_mode}})),
+        "protocol": protocol_note(a),
+        "wall_ms_per_step_incl_flush": round(wall * 1e3 / a.steps, 4),
+        "mean_ms_per_step": round(float(st.sum(1).mean()), 4),
         "stages_ms": {"score": round(t_score, 4), "select": round(t_select, 4),
                       "attn": round(t_attn, 4)},
         "score_select_share": round((t_score + t_select) / stage_sum, 4),
         "density": round(density, 5),
+        "computed_blocks": computed_blocks,
         "dense_ms": None if dense_ms is None else round(dense_ms, 3),
         "speedup_vs_dense": None if dense_ms is None else round(dense_ms / ms_step, 3),
-        "attn_mfma_frac_computed_blocks": round(attn_flops / (t_attn * 1e-3) / 1e12 /
+        "attn_mfma_frac_computed_blocks": round(a_flops / (t_attn * 1e-3) / 1e12 /
                                                 PEAK_BF16_TFLOPS, 4),
-        "score_mfma_frac": round(score_flops / (t_score * 1e-3) / 1e12 / PEAK_BF16_TFLOPS, 4),
-        # K/V (+ Q, O) stream of the attention kernel: profiled HBM bytes per launch / time
-        "attn_hbm_GBps": (None if attn_traffic is None else
-                          round(attn_traffic / (t_attn * 1e-3) / 1e9, 1)),
+        "score_mfma_frac": round(s_flops / (t_score * 1e-3) / 1e12 / PEAK_BF16_TFLOPS, 4),
         "roofline": roofline,
+        "roofline_other": roofline_of(other, kernels[other][0], kernels[other][1],
+                                      other_traffic),
+        "gather_probe": probe,
+        "clock": clk,
+        "env": env_info(),
         "cpu_baseline": cpu,
     }
     if prediction is not None:

@@ -163,7 +163,10 @@ int xattn_select_ratio(const float *scores, const xattn_dims *dims, int block,
  *   o   bf16 [HQ][L][D] (output)
  *   lse fp32 [HQ][L] (output) or NULL
  * QK^T and PV run on the bf16 matrix cores with fp32 accumulation; the
- * online softmax is fp32 and P is rounded to bf16 for the PV product.
+ * online softmax is fp32 and P is rounded to bf16 for the PV product. The
+ * normaliser sums the same rounded P (so o is a weighted mean of the values
+ * with consistent weights); lse carries that rounding, at most 2^-8 relative
+ * in the sum, i.e. below 0.004 in lse.
  */
 int xattn_block_sparse_attn(const void *q, const void *k, const void *v,
                             const xattn_dims *dims, int block, const int32_t *idx,

@@ -1,4 +1,5 @@
-"""Build the gfx950 XAttention library in-tree: paper_2503_16428_amd/lib/libxattn.so.
+"""Build the gfx950 XAttention library in-tree: paper_2503_16428_amd/lib/libxattn.so,
+and the benchmark's measurement probe: paper_2503_16428_amd/lib/libxattn_probe.so.
 
 Every source is compiled by hipcc for gfx950 only. Packed-fp32 instructions
 are disabled (-packed-fp32-ops): hipcc otherwise forms v_pk_* fp32 ops from
@@ -15,7 +16,9 @@ ROOT = os.path.dirname(HERE)
 CSRC = os.path.join(HERE, "csrc")
 OUT_DIR = os.path.join(HERE, "lib")
 LIB = os.path.join(OUT_DIR, "libxattn.so")
+PROBE_LIB = os.path.join(OUT_DIR, "libxattn_probe.so")
 SOURCES = ["score.hip", "select.hip", "attn.hip", "error.hip", "api.cpp", "threshold.cpp"]
+PROBE_SOURCES = ["gather_probe.hip"]
 ARCH = "gfx950"
 
 COMMON_FLAGS = [
@@ -50,13 +53,14 @@ def build(verbose: bool = False, extra_flags: tuple = ()) -> str:
             print(r.stderr, flush=True)
         return obj
 
-    with ThreadPoolExecutor(min(8, len(SOURCES))) as ex:
-        objs = list(ex.map(compile_one, SOURCES))
-    cmd = [hipcc, "-shared", "-fPIC", f"--offload-arch={ARCH}", *objs, "-o", LIB + ".tmp"]
-    if verbose:
-        print(" ".join(cmd), flush=True)
-    subprocess.run(cmd, check=True)
-    os.replace(LIB + ".tmp", LIB)
+    with ThreadPoolExecutor(min(8, len(SOURCES) + len(PROBE_SOURCES))) as ex:
+        objs = list(ex.map(compile_one, SOURCES + PROBE_SOURCES))
+    for lib, lib_objs in ((LIB, objs[:len(SOURCES)]), (PROBE_LIB, objs[len(SOURCES):])):
+        cmd = [hipcc, "-shared", "-fPIC", f"--offload-arch={ARCH}", *lib_objs, "-o", lib + ".tmp"]
+        if verbose:
+            print(" ".join(cmd), flush=True)
+        subprocess.run(cmd, check=True)
+        os.replace(lib + ".tmp", lib)
     return LIB
 
 

@@ -8,7 +8,8 @@
 //   online softmax in fp32 in the log2 domain (lane = query, so the row
 //   max / sum need one cross-half exchange), with lazy rescaling,
 //   O^T += V_h^T P^T    (P rounded to bf16; the key order inside each
-//   16-key MFMA step is permuted so that P never leaves registers).
+//   16-key MFMA step is permuted so that P never leaves registers; the row
+//   sum l adds the same rounded P, so O / l normalises consistently).
 // Keeping the accumulators transposed (lane = query) makes the per-query
 // rescale a lane-local multiply.
 //
@@ -64,6 +65,12 @@ __device__ __forceinline__ float lane_max(const f32x16 (&s)[2]) {
 
 __device__ __forceinline__ uint32_t cvt_pk_bf16(float a, float b) {
   return __builtin_bit_cast(uint32_t, __builtin_convertvector(f32v2{a, b}, bf16v2));
+}
+
+// acc + the two bf16 values packed in pk (one v_dot2c_f32_bf16 against 1.0, 1.0)
+__device__ __forceinline__ float sum_pk_bf16(uint32_t pk, float acc) {
+  return __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16v2, pk),
+                                         __builtin_bit_cast(bf16v2, 0x3F803F80u), acc, false);
 }
 
 // Element offset of logical 16-byte chunk c of row r in a swizzled [64][128]
@@ -273,19 +280,24 @@ __device__ __forceinline__ void attn_body(
     // ---- one scheduling region: S(i+1) MFMAs beside the exponentials of i,
     // then PV(i)
     qk(PAR ^ 1, sn, prefetch);
+    // The row sum adds the bf16-rounded probabilities that the PV product
+    // uses, so O / l is a weighted mean with consistent weights: a query
+    // whose mass sits on one key gets that key's value exactly (up to the
+    // output rounding), whatever the rounding of its probability.
     uint32_t pk[2][8];
-    float ls = 0.f;
+    float ls[2] = {0.f, 0.f};
 #pragma unroll
     for (int kt = 0; kt < 2; ++kt) {
 #pragma unroll
       for (int r = 0; r < 16; r += 2) {
         const float p0 = fast_exp2(fmaf(sc[kt][r], scale_log2, neg_m));
         const float p1 = fast_exp2(fmaf(sc[kt][r + 1], scale_log2, neg_m));
-        ls += p0 + p1;
-        pk[kt][r >> 1] = cvt_pk_bf16(p0, p1);
+        const uint32_t pp = cvt_pk_bf16(p0, p1);
+        pk[kt][r >> 1] = pp;
+        ls[kt] = sum_pk_bf16(pp, ls[kt]);
       }
     }
-    l_run += ls;
+    l_run += ls[0] + ls[1];
     // O^T += V^T P^T. MFMA step u covers keys 16u .. 16u+15 of the half-tile;
     // slot 8 lh + jj of both operands is key 16u + 8 (jj/4) + 4 lh + jj%4.
     const uint16_t* Vb = Vs + PAR * kHalfElems;

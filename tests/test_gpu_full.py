@@ -9,8 +9,8 @@ import pytest
 import oracle
 import workloads as W
 
-from .helpers import (OUT_MAX_ABS, OUT_MEAN_ABS, compare_index_sets, compare_scores,
-                      dev_bf16, host_f32, logit_error_bound, score_tolerance)
+from .helpers import (OUT_MAX_ABS, OUT_MEAN_ABS, assert_attention_on_lists,
+                      assert_index_sets, compare_scores, dev_bf16, host_f32, logit_error_bound)
 
 pytestmark = pytest.mark.gpu
 
@@ -47,30 +47,50 @@ def sample_rows(w, n_heads=3):
     return rh, rb
 
 
+def worst_output_rows(w, g, n):
+    """The n (head, query block) rows holding the largest |o| of the GPU
+    output: where the bf16 rounding of the output and of P costs the most."""
+    NB = w.n_blocks
+    m = g["o"].view(-1, NB, w.block * w.head_dim).abs().amax(-1).float().view(-1)
+    top = torch.topk(m, n).indices.cpu().numpy()
+    return (top // NB).astype(np.int32), (top % NB).astype(np.int32)
+
+
+def with_rows(rows, extra):
+    seen = set(zip(*rows))
+    add = [(h, b) for h, b in zip(*extra) if (h, b) not in seen]
+    if not add:
+        return rows
+    rh = np.concatenate([rows[0], np.array([h for h, _ in add], np.int32)])
+    rb = np.concatenate([rows[1], np.array([b for _, b in add], np.int32)])
+    return rh, rb
+
+
 def check_sampled(w, x, g, rows):
+    """Scores, index lists and outputs of the given rows against the oracle:
+    scores to the asserted bound; index lists exact up to margin / tie
+    explained rows (reported, capped); the attention of every row against the
+    oracle run on the GPU's own lists; end to end against the oracle's whole
+    pipeline on the rows whose lists agree (the others are counted)."""
     rh, rb = rows
     NB = w.n_blocks
     f = oracle.forward_rows(x["q"], x["k"], x["v"], w.block, w.stride, w.tau, w.causal,
                             rows=rows)
     sc = g["scores"].cpu().numpy().reshape(-1, NB, NB)[rh, rb]
-    dz = logit_error_bound(x["q"], x["k"], w.stride, rh, rb, w.hq // w.hkv, w.block)
+    dz = logit_error_bound(x["q"], x["k"], w.stride, rh[:4], rb[:4], w.hq // w.hkv, w.block)
     rep = compare_scores(sc, f["scores"], dz)
     print(f"  {w.name} S={w.stride} tau={w.tau}: scores {rep}", flush=True)
     assert rep["n_bad"] == 0
     gi = g["idx"].cpu().numpy().reshape(-1, NB, NB)[rh, rb]
     gc = g["cnt"].cpu().numpy().reshape(-1, NB)[rh, rb]
-    n_eq, n_m, n_t, bad = compare_index_sets(gi, gc, f["idx"], f["cnt"], f["scores"], rb,
-                                             w.tau, w.causal, score_tolerance(dz)[0])
-    print(f"  index rows: equal={n_eq} margin={n_m} tie={n_t} bad={len(bad)}", flush=True)
-    assert not bad, bad[:3]
-    same = np.array([np.array_equal(gi[r, :gc[r]], f["idx"][r, :f["cnt"][r]])
-                     for r in range(len(rh))])
+    same = assert_index_sets(gi, gc, f["idx"], f["cnt"], f["scores"], rb, w.tau, w.causal)
     o = host_f32(g["o"]).reshape(-1, w.seq, w.head_dim)
     og = np.stack([o[h, b * w.block:(b + 1) * w.block] for h, b in zip(rh, rb)])
+    assert_attention_on_lists(x, w.block, gi, gc, w.causal, rows, og)
     err = np.abs(og[same].astype(np.float64) - f["o"][same])
-    print(f"  output on {same.sum()}/{len(rh)} rows: max_abs={err.max():.3e} "
-          f"mean_abs={err.mean():.3e}", flush=True)
-    assert same.sum() >= len(rh) // 2
+    print(f"  end to end on {same.sum()}/{len(rh)} rows with the oracle's lists "
+          f"({len(rh) - same.sum()} rows with explained list differences): "
+          f"max_abs={err.max():.3e} mean_abs={err.mean():.3e}", flush=True)
     assert err.max() <= OUT_MAX_ABS and err.mean() <= OUT_MEAN_ABS
 
 
@@ -97,7 +117,11 @@ def test_full_size_workload(name):
     x = W.generate(w, threads=16)
     g = run_path(w, x)
     check_properties(w, g)
-    rows = (oracle.all_rows(w.hq, w.n_blocks) if name == "c1" else sample_rows(w))
+    if name == "c1":
+        rows = oracle.all_rows(w.hq, w.n_blocks)
+    else:
+        # position-chosen rows plus the rows holding the largest outputs
+        rows = with_rows(sample_rows(w), worst_output_rows(w, g, 6))
     check_sampled(w, x, g, rows)
     # repeated launches at full size are bitwise identical (no LDS races)
     g2 = run_path(w, x)
@@ -131,7 +155,7 @@ def test_c4_sweep_point(tau, S):
         assert err.max() <= OUT_MAX_ABS and err.mean() <= OUT_MEAN_ABS
     else:
         rh, rb = sample_rows(w, n_heads=2)
-        check_sampled(w, x, g, (rh[::2], rb[::2]))
+        check_sampled(w, x, g, with_rows((rh[::2], rb[::2]), worst_output_rows(w, g, 2)))
 
 
 _C4 = {}

@@ -9,8 +9,7 @@ import pytest
 import oracle
 import workloads as W
 
-from .helpers import compare_index_sets, compare_scores, dev_bf16, logit_error_bound, \
-    score_tolerance
+from .helpers import assert_index_sets, compare_scores, dev_bf16, logit_error_bound
 
 pytestmark = pytest.mark.gpu
 
@@ -86,9 +85,7 @@ def test_patterns_on_the_128k_layer():
         gi = idx.cpu().numpy().reshape(-1, NB)[rh * NB + rb]
         gc = cnt.cpu().numpy().reshape(-1)[rh * NB + rb]
         oi, oc = oracle.select_rows(want, rb, w.tau)
-        _, _, _, bad = compare_index_sets(gi, gc, oi, oc, want, rb, w.tau, True,
-                                          score_tolerance(dz)[0])
-        assert not bad, (pattern, bad[:2])
+        assert_index_sets(gi, gc, oi, oc, want, rb, w.tau, True, tag=f"{pattern} ")
         cov = np.mean([true_mass[r, gi[r, :gc[r]]].sum() for r in range(len(rh))])
         c_all = cnt.cpu().numpy().astype(np.int64)
         dens = c_all.sum() / (np.arange(1, NB + 1).sum() * dims.heads)
