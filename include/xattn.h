@@ -198,6 +198,28 @@ int xattn_forward(const void *q, const void *k, const void *v, const xattn_dims 
                   void *workspace, size_t workspace_bytes, void *stream);
 
 /*
+ * xattn_forward without allocation, for callers that cannot allocate device
+ * memory: code under HIP graph capture, tight serving loops, harnesses that
+ * forbid hipMalloc. The workspace of xattn_forward lives in a static device
+ * array of XATTN_NOALLOC_SCRATCH_BYTES bytes that the library owns (one per
+ * GPU, held until the process ends; its address is looked up once per device
+ * on the first call with that device current). The caller passes inputs and
+ * outputs only; the call makes no allocation of any kind.
+ *   Everything else as xattn_forward (o, lse and their meaning; results
+ *   bitwise equal to xattn_forward's on the same inputs).
+ * Errors: as xattn_forward, plus XATTN_ERR_UNSUPPORTED when the problem needs
+ * more scratch than the static array holds (xattn_forward_workspace_size()
+ * > XATTN_NOALLOC_SCRATCH_BYTES), and XATTN_ERR_HIP if the array's address
+ * cannot be obtained.
+ * Every call on one GPU shares that GPU's array, which keeps the last call's
+ * contents: calls that overlap on one GPU (several streams or threads at
+ * once) race and must be serialised by the caller.
+ */
+#define XATTN_NOALLOC_SCRATCH_BYTES ((size_t)64 << 20)
+int xattn_forward_noalloc(const void *q, const void *k, const void *v, const xattn_dims *dims,
+                          int block, int stride, float tau, void *o, float *lse, void *stream);
+
+/*
  * Denoising-step schedule of the video-generation experiment (Sec. 4.2):
  * dense attention for the first warmup_steps steps of a diffusion sampler
  * (step < warmup_steps; the paper uses 5 of 50), XAttention from then on.

@@ -7,7 +7,8 @@ from .binding import (  # noqa: F401
     BLOCK, Dims, XAttnError, forward_layout, forward_workspace_size, head_error,
     head_error_mean, lib, lib_path, make_dims, score_workspace_size, threshold_dp,
     threshold_levels, threshold_predict, version,
-    xattn_block_sparse_attn, xattn_dense_attn, xattn_forward, xattn_forward_scheduled,
+    xattn_block_sparse_attn, xattn_dense_attn, xattn_forward, xattn_forward_noalloc,
+    xattn_forward_scheduled,
     xattn_score, xattn_score_pattern, xattn_select, xattn_select_heads, xattn_select_ratio,
     xattn_select_topk,
 )

@@ -60,7 +60,7 @@ EXPORTS = [
     "xattn_select_heads",
     "xattn_select_topk", "xattn_select_ratio", "xattn_block_sparse_attn",
     "xattn_dense_attn", "xattn_forward_workspace_size", "xattn_forward_layout",
-    "xattn_forward", "xattn_forward_scheduled", "xattn_threshold_dp",
+    "xattn_forward", "xattn_forward_noalloc", "xattn_forward_scheduled", "xattn_threshold_dp",
     "xattn_threshold_levels", "xattn_threshold_predict",
     "xattn_head_error_workspace_size", "xattn_head_error", "xattn_head_error_mean",
     "xattn_strerror", "xattn_last_error", "xattn_version",
@@ -93,6 +93,7 @@ def lib() -> ctypes.CDLL:
         L.xattn_forward_workspace_size.argtypes = [PD, I, I, PSZ]
         L.xattn_forward_layout.argtypes = [PD, I, I, PSZ, PSZ, PSZ, PSZ]
         L.xattn_forward.argtypes = [P, P, P, PD, I, I, F, P, P, P, SZ, P]
+        L.xattn_forward_noalloc.argtypes = [P, P, P, PD, I, I, F, P, P, P]
         L.xattn_forward_scheduled.argtypes = [P, P, P, PD, I, I, F, I, I, P, P, P, SZ, P]
         L.xattn_threshold_dp.argtypes = [P, I, I, I, P, P]
         L.xattn_threshold_levels.argtypes = [ctypes.c_double, I, P]
@@ -391,6 +392,21 @@ def xattn_forward(q, k, v, causal=True, block=BLOCK, stride=8, tau=0.9, o=None, 
                                float(tau), _ptr(o), _ptr(lse), _ptr(workspace),
                                workspace.numel(), _stream(stream)))
     return o, lse, _forward_views(workspace, d, block, stride)
+
+
+def xattn_forward_noalloc(q, k, v, o, lse=None, causal=True, block=BLOCK, stride=8, tau=0.9,
+                          stream=None):
+    """score -> select -> sparse attention with the library's static scratch
+    (no allocation by the call): the caller passes the output o (bf16 like q)
+    and optionally lse (fp32 [H, seq]). Returns (o, lse)."""
+    d = _qkv_dims(q, k, v, causal)
+    if o is None:
+        raise XAttnError(XATTN_ERR_ARG, "o must be given (the call allocates nothing)")
+    _check_outputs(q, d, o, lse)
+    _on_device(q=q, k=k, v=v, o=o, lse=lse)
+    _check(lib().xattn_forward_noalloc(_ptr(q), _ptr(k), _ptr(v), ctypes.byref(d), block,
+                                       stride, float(tau), _ptr(o), _ptr(lse), _stream(stream)))
+    return o, lse
 
 
 def xattn_forward_scheduled(q, k, v, step, warmup_steps=5, causal=False, block=BLOCK,

@@ -17,7 +17,8 @@ CSRC = os.path.join(HERE, "csrc")
 OUT_DIR = os.path.join(HERE, "lib")
 LIB = os.path.join(OUT_DIR, "libxattn.so")
 PROBE_LIB = os.path.join(OUT_DIR, "libxattn_probe.so")
-SOURCES = ["score.hip", "select.hip", "attn.hip", "error.hip", "api.cpp", "threshold.cpp"]
+SOURCES = ["score.hip", "select.hip", "attn.hip", "error.hip", "noalloc.hip", "api.cpp",
+           "threshold.cpp"]
 PROBE_SOURCES = ["gather_probe.hip"]
 ARCH = "gfx950"
 

@@ -309,6 +309,29 @@ int xattn_forward(const void* q, const void* k, const void* v, const xattn_dims*
   return hip_status(e, "xattn_forward launch");
 }
 
+int xattn_forward_noalloc(const void* q, const void* k, const void* v, const xattn_dims* dims,
+                          int block, int stride, float tau, void* o, float* lse, void* stream) {
+  static_assert(kNoallocScratchBytes == XATTN_NOALLOC_SCRATCH_BYTES, "header and library agree");
+  XattnShape s;
+  int rc;
+  if ((rc = check_dims(dims, &s)) || (rc = check_block(block)) || (rc = check_stride(stride)) ||
+      (rc = check_tau(tau)))
+    return rc;
+  if (!q || !k || !v || !o) return fail(XATTN_ERR_ARG, "q, k, v and o must be non-NULL");
+  size_t need = 0;
+  if ((rc = xattn_forward_workspace_size(dims, block, stride, &need))) return rc;
+  if (need > kNoallocScratchBytes)
+    return fail(XATTN_ERR_UNSUPPORTED,
+                "this problem needs %zu bytes of scratch; xattn_forward_noalloc holds %zu "
+                "(use xattn_forward with a caller workspace)",
+                need, kNoallocScratchBytes);
+  void* ws = nullptr;
+  if (hipError_t e = noalloc_scratch(&ws); e != hipSuccess)
+    return hip_status(e, "xattn_forward_noalloc: address of the static scratch");
+  return xattn_forward(q, k, v, dims, block, stride, tau, o, lse, ws, kNoallocScratchBytes,
+                       stream);
+}
+
 int xattn_forward_scheduled(const void* q, const void* k, const void* v, const xattn_dims* dims,
                             int block, int stride, float tau, int step, int warmup_steps,
                             void* o, float* lse, void* workspace, size_t workspace_bytes,

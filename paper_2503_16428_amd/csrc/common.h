@@ -99,3 +99,8 @@ hipError_t launch_head_error(const void* o, const void* o_ref, const XattnShape&
 hipError_t launch_attn(const void* q, const void* k, const void* v, const XattnShape& s,
                        const int32_t* idx, const int32_t* cnt, bool dense, void* o,
                        float* lse, hipStream_t st);
+// The static scratch of xattn_forward_noalloc (XATTN_NOALLOC_SCRATCH_BYTES
+// bytes per device): its device address on the current device, fetched on
+// the first call per device.
+constexpr size_t kNoallocScratchBytes = (size_t)64 << 20;
+hipError_t noalloc_scratch(void** ptr);

@@ -175,3 +175,19 @@ def test_pattern_scoring_validates_before_launch():
     a = (ctypes.c_int32 * 8)(*range(8))
     assert L.xattn_score_pattern(fake, fake, ctypes.byref(d), 128, 8, a, fake, None, 0,
                                  None) == B.XATTN_ERR_WORKSPACE
+
+
+def test_noalloc_forward_validates_before_any_hip_call():
+    L = X.lib()
+    fake = ctypes.c_void_p(0x1000)   # never dereferenced: every case fails validation
+    d = _dims()
+    assert L.xattn_forward_noalloc(fake, fake, None, ctypes.byref(d), 128, 8, 0.9, fake, None,
+                                   None) == B.XATTN_ERR_ARG
+    assert L.xattn_forward_noalloc(fake, fake, fake, ctypes.byref(d), 128, 8, 0.0, fake, None,
+                                   None) == B.XATTN_ERR_ARG
+    assert L.xattn_forward_noalloc(fake, fake, fake, ctypes.byref(d), 128, 3, 0.9, fake, None,
+                                   None) == B.XATTN_ERR_ARG
+    big = _dims(hq=32, hkv=8, seq=32768)
+    assert L.xattn_forward_noalloc(fake, fake, fake, ctypes.byref(big), 128, 8, 0.9, fake, None,
+                                   None) == B.XATTN_ERR_UNSUPPORTED
+    assert b"scratch" in L.xattn_last_error()
