@@ -209,54 +209,49 @@ def cpu_info():
     return {"cpu_model": model, "affinity_cpus": len(os.sched_getaffinity(0))}
 
 
-class ClockSampler:
-    """The GPU shader (GFX) clock read through amdsmi on a host thread every
-    few milliseconds while the timed region runs; reports the median in MHz
-    (None, with the reason, where amdsmi cannot read it)."""
+class ShaderClock:
+    """Mean shader clock per XCD over the timed region: the probe library's
+    clock kernel (64 workgroups, so every XCD) runs on the launch stream
+    right before the first and right after the last timed step and reads the
+    shader-cycle and constant-rate counters; per XCD, clock = cycles / (ticks
+    / tick rate)."""
 
-    def __init__(self, period_s=0.002):
-        self.period, self.samples, self.error = period_s, [], None
-        self._stop = threading.Event()
-        self._thr = None
+    def __init__(self, stream, n_wg=64):
+        import torch
+        from paper_2503_16428_amd import build as B
+        self.stream, self.n_wg, self.error = stream, n_wg, None
+        self.buf = torch.zeros((2, 3 * n_wg), dtype=torch.int64, device="cuda")
         try:
-            import amdsmi
-            amdsmi.amdsmi_init()
-            self._smi = amdsmi
-            self._h = amdsmi.amdsmi_get_processor_handles()[0]
-            self._read()
-        except Exception as e:  # noqa: BLE001
-            self.error = f"{type(e).__name__}: {e}"
+            self.lib = ctypes.CDLL(B.PROBE_LIB)
+            self.lib.xattn_probe_clock.argtypes = [ctypes.c_void_p, ctypes.c_int, ctypes.c_void_p]
+            self.khz = self.lib.xattn_probe_wall_clock_khz()
+        except OSError as e:
+            self.lib, self.error = None, f"probe library: {e}"
 
-    def _read(self):
-        info = self._smi.amdsmi_get_clock_info(self._h, self._smi.AmdSmiClkType.GFX)
-        return float(info["clk"])
+    def sample(self, i):
+        if self.lib is None:
+            return
+        rc = self.lib.xattn_probe_clock(ctypes.c_void_p(self.buf[i].data_ptr()), self.n_wg,
+                                        ctypes.c_void_p(self.stream.cuda_stream))
+        if rc != 0:
+            self.error = f"clock probe launch failed ({rc})"
 
-    def _run(self):
-        while not self._stop.is_set():
-            try:
-                self.samples.append(self._read())
-            except Exception as e:  # noqa: BLE001
-                self.error = f"{type(e).__name__}: {e}"
-                return
-            time.sleep(self.period)
-
-    def start(self):
-        if self.error is None:
-            self._thr = threading.Thread(target=self._run, daemon=True)
-            self._thr.start()
-
-    def stop(self):
-        if self._thr is not None:
-            self._stop.set()
-            self._thr.join()
-        if self.error is None:
-            try:
-                self._smi.amdsmi_shut_down()
-            except Exception:  # noqa: BLE001
-                pass
-        return {"gfx_clock_mhz_median": median(self.samples) if self.samples else None,
-                "gfx_clock_samples": len(self.samples), "source": "amdsmi GFX clk",
-                "error": self.error}
+    def result(self):
+        if self.lib is None or self.error or not self.khz:
+            return {"shader_clock_mhz": None, "error": self.error or "no tick rate"}
+        b = self.buf.cpu().numpy().reshape(2, self.n_wg, 3)
+        per = {}
+        for x in sorted(set(b[0, :, 0].tolist()) & set(b[1, :, 0].tolist())):
+            r0 = b[0][b[0, :, 0] == x][0]
+            r1 = b[1][b[1, :, 0] == x][0]
+            ticks = float(r1[2] - r0[2])
+            if ticks > 0:
+                per[int(x)] = (r1[1] - r0[1]) / (ticks / (self.khz * 1e3)) / 1e6
+        mhz = [per[x] for x in sorted(per)]
+        return {"shader_clock_mhz": round(float(np.mean(mhz)), 1) if mhz else None,
+                "per_xcd_mhz": [round(m, 1) for m in mhz],
+                "source": "s_memtime / s_memrealtime across the timed region",
+                "tick_rate_khz": self.khz}
 
 
 # ---------------------------------------------------------------- GPU legs
@@ -284,10 +279,11 @@ class Flusher:
             self.buf.fill_(self.n)
 
 
-def time_steps(stages, steps, warmup, stream, flush):
+def time_steps(stages, steps, warmup, stream, flush, clock=None):
     """Run warmup untimed steps, then `steps` timed ones (flush before each,
-    HIP events around each stage on the launch stream). Returns (per-stage
-    event times [steps][n_stages] in ms, wall seconds of the timed steps)."""
+    HIP events around each stage on the launch stream; the shader clock
+    sampled before the first and after the last). Returns (per-stage event
+    times [steps][n_stages] in ms, wall seconds of the timed steps)."""
     import torch
     for _ in range(warmup):
         for f in stages:
@@ -296,12 +292,16 @@ def time_steps(stages, steps, warmup, stream, flush):
     evs = [[torch.cuda.Event(enable_timing=True) for _ in range(len(stages) + 1)]
            for _ in range(steps)]
     t0 = time.perf_counter()
+    if clock is not None:
+        clock.sample(0)
     for i in range(steps):
         flush()
         evs[i][0].record(stream)
         for j, f in enumerate(stages):
             f()
             evs[i][j + 1].record(stream)
+    if clock is not None:
+        clock.sample(1)
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
     st = np.array([[e[j].elapsed_time(e[j + 1]) for j in range(len(stages))] for e in evs])
@@ -416,8 +416,7 @@ def sweep_main(a, w, q, k, v, dims, stream, flush, x):
     o = torch.empty_like(q)
     points = []
     dflops = dense_flops(w)
-    clock = ClockSampler()
-    clock.start()
+    clocks = []
     for tau, S in W.C4_SWEEP:
         wp = w.with_(tau=tau, stride=S)
         ws = torch.empty(X.score_workspace_size(dims, w.block, S), dtype=torch.uint8,
@@ -428,7 +427,10 @@ def sweep_main(a, w, q, k, v, dims, stream, flush, x):
             lambda: X.xattn_block_sparse_attn(q, k, v, idx, cnt, w.causal, w.block, o=o,
                                               want_lse=False),
         ]
-        st, wall = time_steps(stages, a.steps, a.warmup, stream, flush)
+        clock = ShaderClock(stream)
+        st, wall = time_steps(stages, a.steps, a.warmup, stream, flush, clock)
+        clk = clock.result()
+        clocks.append(clk["shader_clock_mhz"])
         t_score, t_select, t_attn = (median(st[:, j]) for j in range(3))
         ms = median(st.sum(1))
         c = cnt.cpu().numpy().astype(np.int64)
@@ -440,13 +442,12 @@ def sweep_main(a, w, q, k, v, dims, stream, flush, x):
             "tau": tau, "stride": S, "ms_per_step": round(ms, 4),
             "stages_ms": {"score": round(t_score, 4), "select": round(t_select, 4),
                           "attn": round(t_attn, 4)},
-            "density": round(dens, 5),
+            "density": round(dens, 5), "shader_clock_mhz": clk["shader_clock_mhz"],
             "dense_equiv_tflops": round(dflops / (ms * 1e-3) / 1e12, 1),
             "score_select_share": round((t_score + t_select) / (t_score + t_select + t_attn), 4),
             "roofline_attn": roofline_of("attn", attn_flops(blocks, w), t_attn, tr_a),
             "roofline_score": roofline_of("score", score_flops(wp), t_score, tr_s)})
         print(f"# tau={tau} S={S}: {ms:.3f} ms, density {dens:.4f}", file=sys.stderr, flush=True)
-    clk = clock.stop()
     ref = next(p for p in points if p["tau"] == 0.9 and p["stride"] == w.stride)
     dom = "attn" if ref["stages_ms"]["attn"] >= ref["stages_ms"]["score"] else "score"
     cpu = None
@@ -462,7 +463,7 @@ def sweep_main(a, w, q, k, v, dims, stream, flush, x):
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "bf16",
         "data": "synthetic",
         "config": dict(w.describe(), sweep="tau x S; value at tau=0.9, S=8"),
-        "protocol": protocol_note(a), "clock": clk, "env": env_info(),
+        "protocol": protocol_note(a), "env": env_info(),
         "sweep": points, "roofline": ref[f"roofline_{dom}"], "cpu_baseline": cpu,
     }
     print(json.dumps(out), flush=True)
@@ -606,10 +607,9 @@ def main(argv=None):
     def attend():
         X.xattn_block_sparse_attn(q, k, v, idx, cnt, w.causal, w.block, o=o, want_lse=False)
 
-    clock = ClockSampler()
-    clock.start()
-    st, wall = time_steps([score, select, attend], a.steps, a.warmup, stream, flush)
-    clk = clock.stop()
+    clock = ShaderClock(stream)
+    st, wall = time_steps([score, select, attend], a.steps, a.warmup, stream, flush, clock)
+    clk = clock.result()
     print(f"# timed {a.steps} steps in {wall:.2f} s", file=sys.stderr, flush=True)
     t_score, t_select, t_attn = (median(st[:, j]) for j in range(3))
     ms_step = median(st.sum(1))

@@ -19,7 +19,7 @@ LIB = os.path.join(OUT_DIR, "libxattn.so")
 PROBE_LIB = os.path.join(OUT_DIR, "libxattn_probe.so")
 SOURCES = ["score.hip", "select.hip", "attn.hip", "error.hip", "noalloc.hip", "api.cpp",
            "threshold.cpp"]
-PROBE_SOURCES = ["gather_probe.hip"]
+PROBE_SOURCES = ["probe.hip"]
 ARCH = "gfx950"
 
 COMMON_FLAGS = [

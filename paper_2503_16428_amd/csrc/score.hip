@@ -19,13 +19,14 @@
 #include <atomic>
 
 #include "common.h"
+#include "score_rows.h"
 
 using namespace xattn;
 
 namespace {
 
 constexpr int TM = 256;             // reduced rows (R) and columns (c) per workgroup tile
-constexpr int TSUB = 128;           // column sub-tile owning one (m, l) pair per row
+constexpr int TSUB = kTsub;         // column sub-tile owning one (m, l) pair per row
 constexpr int KC = 64;              // reduced-K chunk per pipeline stage (128-byte rows)
 constexpr int NSTAGE = 2;           // stages: one chunk computed while the next loads
 constexpr int kThreads = 512;       // 8 waves: 2 (columns) x 4 (rows), 128 c x 64 R each
@@ -239,11 +240,16 @@ __global__ __launch_bounds__(kThreads, 1) void score_partials(
       }
       const float l = lloc + __shfl_xor(lloc, 32);
       const bool rvalid = R < NR;
-      // part is [head][query block][key block][row in block]: what the
+      // part is [head][query block][key block][row in block] (causal: key
+      // blocks <= the query block only, rows packed as a triangle): what the
       // finalize workgroup of one query block reads is one contiguous slab;
       // a half-wave writes 32 / NRB runs of NRB consecutive floats per block.
       const int Rv = rvalid ? R : 0;
-      float* pcol = part + ((size_t)(h * NB + Rv / NRB) * NB) * NRB + (Rv % NRB);
+      const int qb = Rv / NRB;
+      float* pcol = part + part_row(h, qb, NB, CAUSAL) * NRB + (Rv % NRB);
+      // key block j of this row is stored if it exists and, when causal, is
+      // not above the diagonal (those are fully masked and have no slot)
+      auto keep = [&](int j) { return rvalid && j < NB && (!CAUSAL || j <= qb); };
   
       if constexpr (NRB >= 8) {
         // group gi covers columns 8 gi + 4 lh + [0, 4): local block gi / (NRB / 8)
@@ -263,39 +269,38 @@ __global__ __launch_bounds__(kThreads, 1) void score_partials(
           for (int x = 0; x < NBL / 2; ++x) {
             const float tot = half_pair_sum(block_sum(x), block_sum(NBL / 2 + x));
             const int jb = lh * (NBL / 2) + x;
-            if (rvalid && j0 + jb < NB) pcol[(size_t)(j0 + jb) * NRB] = tot;
+            if (keep(j0 + jb)) pcol[(size_t)(j0 + jb) * NRB] = tot;
           }
         } else {
           const float s0 = block_sum(0);
           const float tot = half_pair_sum(s0, s0);
-          if (rvalid && lh == 0 && j0 < NB) pcol[(size_t)j0 * NRB] = tot;
+          if (lh == 0 && keep(j0)) pcol[(size_t)j0 * NRB] = tot;
         }
       } else if constexpr (NRB == 4) {
         // each group of 4 columns is one block: local block 2 gi + lh
-        if (rvalid) {
   #pragma unroll
-          for (int gi = 0; gi < 16; ++gi) {
-            const int j = j0 + 2 * gi + lh;
-            if (j < NB) pcol[(size_t)j * NRB] = gsum[gi];
-          }
+        for (int gi = 0; gi < 16; ++gi) {
+          const int j = j0 + 2 * gi + lh;
+          if (keep(j)) pcol[(size_t)j * NRB] = gsum[gi];
         }
       } else {  // NRB == 2: each group holds two blocks
         static_assert(NRB == 2, "stride must divide the block");
-        if (rvalid) {
   #pragma unroll
-          for (int t = 0; t < 4; ++t) {
+        for (int t = 0; t < 4; ++t) {
   #pragma unroll
-            for (int g4 = 0; g4 < 4; ++g4) {
-              const int gi = 4 * t + g4;
-              const int j = j0 + 4 * gi + 2 * lh;
-              if (j < NB) pcol[(size_t)j * NRB] = acc[t][n][4 * g4] + acc[t][n][4 * g4 + 1];
-              if (j + 1 < NB) pcol[(size_t)(j + 1) * NRB] = acc[t][n][4 * g4 + 2] + acc[t][n][4 * g4 + 3];
-            }
+          for (int g4 = 0; g4 < 4; ++g4) {
+            const int gi = 4 * t + g4;
+            const int j = j0 + 4 * gi + 2 * lh;
+            if (keep(j)) pcol[(size_t)j * NRB] = acc[t][n][4 * g4] + acc[t][n][4 * g4 + 1];
+            if (keep(j + 1))
+              pcol[(size_t)(j + 1) * NRB] = acc[t][n][4 * g4 + 2] + acc[t][n][4 * g4 + 3];
           }
         }
       }
-      if (rvalid && lh == 0 && tsub_idx < NT)
-        stats[((size_t)h * NT + tsub_idx) * NR + R] = make_float2(m, l);
+      // causal: a sub-tile starting after the row has no stats slot (all its
+      // columns are masked for that row)
+      if (rvalid && lh == 0 && tsub_idx < NT && (!CAUSAL || R >= tsub_idx * TSUB))
+        stats[stats_at(h, tsub_idx, R, NR, NT, CAUSAL)] = make_float2(m, l);
     }
   };
 
@@ -329,130 +334,17 @@ __global__ __launch_bounds__(kThreads, 1) void score_partials(
   wait_vmcnt<0>();  // the last loads land before the LDS is released
 }
 
-__device__ __forceinline__ float wave_max(float x) {
-#pragma unroll
-  for (int off = 32; off >= 1; off >>= 1) x = fmaxf(x, __shfl_xor(x, off));
-  return x;
-}
-__device__ __forceinline__ float wave_sum(float x) {
-#pragma unroll
-  for (int off = 32; off >= 1; off >>= 1) x += __shfl_xor(x, off);
-  return x;
-}
-
-constexpr int kStatMax = 2048;  // (row, tile) stats staged in LDS (16 KB) when they fit
-constexpr int kFinUnroll = 4;   // independent 16-byte partial-sum loads per thread
-
-// One workgroup (4 waves) per (query head, query block) row, nrb = B/S
-// reduced rows R = b nrb + r and tn column sub-tiles per row:
-//   m_R = max_t m[t][R],  l_R = sum_t l[t][R] 2^(m[t][R] - m_R),
-//   f[r][t] = 2^(m[t][R] - m_R) / l_R,
-//   score[h][b][j] = (1/nrb) sum_r part[j][R] f[r][t(j)].
-// The (r, t) stats are read r-fastest (the nrb rows of one tile are adjacent
-// in memory) into LDS; one wave per row reduces them in a fixed order. The
-// row's partial-sum slab [j][r] is streamed as float4 (or float2 when nrb =
-// 2), kFinUnroll loads in flight per thread; the nrb / 4 lanes of one block
-// then reduce with shuffles in a fixed order. Rows whose stats exceed the LDS
-// stage use the same arithmetic with the stats read from global memory.
+// One workgroup (4 waves) per (query head, query block) row: the row's
+// scores from its partial sums and tile statistics (finalize_row).
 template <bool CAUSAL>
-__global__ __launch_bounds__(256) void score_finalize(const float* __restrict__ part,
-                                                      const float2* __restrict__ stats, int NR,
-                                                      int NB, int NT, int nrb,
-                                                      float* __restrict__ scores) {
+__global__ __launch_bounds__(kFinThreads) void score_finalize(const float* __restrict__ part,
+                                                              const float2* __restrict__ stats,
+                                                              int NR, int NB, int NT, int nrb,
+                                                              float* __restrict__ scores) {
+  __shared__ FinalizeLds lds;
   const int h = blockIdx.x / NB, b = blockIdx.x % NB;
-  const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
-  __shared__ float mR[kBlock], ilR[kBlock];
-  __shared__ float sm[kStatMax], sl[kStatMax];  // sm[t * nrb + r]: m, then the factor f
-  const int ncand = CAUSAL ? b + 1 : NB;
-  const int tn = CAUSAL ? (b * nrb) / TSUB + 1 : NT;  // sub-tiles of this row's stats
-  const float2* st = stats + (size_t)h * NT * NR + (size_t)b * nrb;  // + t * NR + r
-  const bool staged = nrb * tn <= kStatMax;
-  if (staged) {
-    for (int i = tid; i < nrb * tn; i += 256) {
-      const int t = i / nrb, r = i - t * nrb;
-      const float2 v = st[(size_t)t * NR + r];
-      sm[i] = v.x;
-      sl[i] = v.y;
-    }
-    __syncthreads();
-  }
-  for (int r = wv; r < nrb; r += 4) {
-    float m = -INFINITY;
-    for (int t = lane; t < tn; t += 64)
-      m = fmaxf(m, staged ? sm[t * nrb + r] : st[(size_t)t * NR + r].x);
-    m = wave_max(m);
-    float l = 0.f;
-    for (int t = lane; t < tn; t += 64) {
-      const float2 v = staged ? make_float2(sm[t * nrb + r], sl[t * nrb + r])
-                              : st[(size_t)t * NR + r];
-      l += v.y * fast_exp2(v.x - m);
-    }
-    l = wave_sum(l);
-    if (lane == 0) {
-      mR[r] = m;
-      ilR[r] = 1.f / l;
-    }
-  }
-  __syncthreads();
-  if (staged) {
-    for (int i = tid; i < nrb * tn; i += 256) {
-      const int r = i % nrb;
-      sm[i] = fast_exp2(sm[i] - mR[r]) * ilR[r];
-    }
-    __syncthreads();
-  }
-  auto factor = [&](int r, int t) -> float {
-    return staged ? sm[t * nrb + r] : fast_exp2(st[(size_t)t * NR + r].x - mR[r]) * ilR[r];
-  };
-
-  const float inv_nrb = 1.f / (float)nrb;
-  float* out = scores + ((size_t)h * NB + b) * NB;
-  const float* pb = part + ((size_t)(h * NB + b) * NB) * nrb;  // this row's slab [j][r]
-  if (nrb >= 4) {
-    // chunk q = 4 consecutive floats = rows 4 (q % (nrb/4)) .. +3 of block q / (nrb/4)
-    const int cpb = nrb / 4;  // chunks (lanes) per block, a power of two <= 32
-    const int nq = ncand * cpb;
-    const float4* p4 = (const float4*)pb;
-    for (int q0 = 0; q0 < nq; q0 += 256 * kFinUnroll) {
-      float4 v[kFinUnroll];
-#pragma unroll
-      for (int u = 0; u < kFinUnroll; ++u) {
-        const int q = q0 + 256 * u + tid;
-        v[u] = q < nq ? p4[q] : make_float4(0.f, 0.f, 0.f, 0.f);
-      }
-#pragma unroll
-      for (int u = 0; u < kFinUnroll; ++u) {
-        const int q = q0 + 256 * u + tid;
-        const int j = q / cpb, r0 = 4 * (q % cpb);
-        const int t = (j * nrb) / TSUB;
-        float acc = 0.f;
-        if (q < nq)
-          acc = v[u].x * factor(r0, t) + v[u].y * factor(r0 + 1, t) +
-                v[u].z * factor(r0 + 2, t) + v[u].w * factor(r0 + 3, t);
-        for (int off = cpb / 2; off >= 1; off >>= 1) acc += __shfl_xor(acc, off);
-        if (q < nq && (q % cpb) == 0) out[j] = acc * inv_nrb;
-      }
-    }
-  } else {  // nrb == 2: one float2 per block
-    const float2* p2 = (const float2*)pb;
-    for (int j0 = 0; j0 < ncand; j0 += 256 * kFinUnroll) {
-      float2 v[kFinUnroll];
-#pragma unroll
-      for (int u = 0; u < kFinUnroll; ++u) {
-        const int j = j0 + 256 * u + tid;
-        v[u] = j < ncand ? p2[j] : make_float2(0.f, 0.f);
-      }
-#pragma unroll
-      for (int u = 0; u < kFinUnroll; ++u) {
-        const int j = j0 + 256 * u + tid;
-        if (j < ncand) {
-          const int t = (j * nrb) / TSUB;
-          out[j] = (v[u].x * factor(0, t) + v[u].y * factor(1, t)) * inv_nrb;
-        }
-      }
-    }
-  }
-  for (int j = ncand + tid; j < NB; j += 256) out[j] = 0.f;  // not candidates
+  finalize_row<CAUSAL>(part, stats, NR, NB, NT, nrb, h, b, scores + ((size_t)h * NB + b) * NB,
+                       lds);
 }
 
 // Compute units of the current device, rounded down to a multiple of the 8
@@ -500,38 +392,50 @@ hipError_t launch_partials_c(const void* q, const void* k, const XattnShape& s,
 }  // namespace
 
 size_t score_scratch_bytes(const XattnShape& s, int stride) {
-  const size_t NR = (size_t)s.seq / stride, NB = s.NB(), NT = ceil_div((int)NR, TSUB);
-  const size_t part = (size_t)s.HQ() * NR * NB * sizeof(float);
-  const size_t stats = (size_t)s.HQ() * NR * NT * 2 * sizeof(float);
+  const int NR = s.seq / stride, NB = s.NB(), NT = ceil_div(NR, TSUB);
+  const size_t part = part_elems(s.HQ(), NB, kBlock / stride, s.causal) * sizeof(float);
+  const size_t stats = (size_t)s.HQ() * stats_per_head(NR, NT, s.causal) * sizeof(float2);
   return ((part + 255) / 256) * 256 + stats;
+}
+
+ScoreScratch score_scratch_views(const XattnShape& s, int stride, void* scratch) {
+  const size_t part_bytes =
+      part_elems(s.HQ(), s.NB(), kBlock / stride, s.causal) * sizeof(float);
+  ScoreScratch v;
+  v.part = (float*)scratch;
+  v.stats = (float*)((char*)scratch + ((part_bytes + 255) / 256) * 256);
+  return v;
+}
+
+hipError_t launch_score_partials(const void* q, const void* k, const XattnShape& s, int stride,
+                                 const int32_t* qsub, void* scratch, hipStream_t st) {
+  SubRowPairing pr;
+  for (int t = 0; t < stride; ++t) pr.q[t] = qsub ? qsub[t] : stride - 1 - t;
+  const ScoreScratch v = score_scratch_views(s, stride, scratch);
+  switch (stride) {
+    case 1: return launch_partials_c<128>(q, k, s, pr, v.part, v.stats, st);
+    case 2: return launch_partials_c<64>(q, k, s, pr, v.part, v.stats, st);
+    case 4: return launch_partials_c<32>(q, k, s, pr, v.part, v.stats, st);
+    case 8: return launch_partials_c<16>(q, k, s, pr, v.part, v.stats, st);
+    case 16: return launch_partials_c<8>(q, k, s, pr, v.part, v.stats, st);
+    case 32: return launch_partials_c<4>(q, k, s, pr, v.part, v.stats, st);
+    case 64: return launch_partials_c<2>(q, k, s, pr, v.part, v.stats, st);
+    default: return hipErrorInvalidValue;
+  }
 }
 
 hipError_t launch_score(const void* q, const void* k, const XattnShape& s, int stride,
                         const int32_t* qsub, float* scores, void* scratch, hipStream_t st) {
-  SubRowPairing pr;
-  for (int t = 0; t < stride; ++t) pr.q[t] = qsub ? qsub[t] : stride - 1 - t;
-  const int NR = s.seq / stride, NB = s.NB(), NT = ceil_div(NR, TSUB);
-  const size_t part_bytes = (size_t)s.HQ() * NR * NB * sizeof(float);
-  float* part = (float*)scratch;
-  float* stats = (float*)((char*)scratch + ((part_bytes + 255) / 256) * 256);
-  hipError_t e;
-  switch (stride) {
-    case 1: e = launch_partials_c<128>(q, k, s, pr, part, stats, st); break;
-    case 2: e = launch_partials_c<64>(q, k, s, pr, part, stats, st); break;
-    case 4: e = launch_partials_c<32>(q, k, s, pr, part, stats, st); break;
-    case 8: e = launch_partials_c<16>(q, k, s, pr, part, stats, st); break;
-    case 16: e = launch_partials_c<8>(q, k, s, pr, part, stats, st); break;
-    case 32: e = launch_partials_c<4>(q, k, s, pr, part, stats, st); break;
-    case 64: e = launch_partials_c<2>(q, k, s, pr, part, stats, st); break;
-    default: return hipErrorInvalidValue;
-  }
+  hipError_t e = launch_score_partials(q, k, s, stride, qsub, scratch, st);
   if (e != hipSuccess) return e;
+  const int NR = s.seq / stride, NB = s.NB(), NT = ceil_div(NR, TSUB);
   const int nrb = kBlock / stride;
+  const ScoreScratch v = score_scratch_views(s, stride, scratch);
   if (s.causal)
-    hipLaunchKernelGGL(score_finalize<true>, dim3(s.HQ() * NB), dim3(256), 0, st, part,
-                       (const float2*)stats, NR, NB, NT, nrb, scores);
+    hipLaunchKernelGGL(score_finalize<true>, dim3(s.HQ() * NB), dim3(kFinThreads), 0, st, v.part,
+                       (const float2*)v.stats, NR, NB, NT, nrb, scores);
   else
-    hipLaunchKernelGGL(score_finalize<false>, dim3(s.HQ() * NB), dim3(256), 0, st, part,
-                       (const float2*)stats, NR, NB, NT, nrb, scores);
+    hipLaunchKernelGGL(score_finalize<false>, dim3(s.HQ() * NB), dim3(kFinThreads), 0, st,
+                       v.part, (const float2*)v.stats, NR, NB, NT, nrb, scores);
   return hipGetLastError();
 }

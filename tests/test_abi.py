@@ -81,8 +81,15 @@ def test_workspace_sizes_cover_partials():
     d = _dims(hq=32, hkv=8, seq=131072)
     rc, n = _score_ws(d, 128, 16)
     assert rc == 0
-    NR, NB = 131072 // 16, 1024
-    assert n >= 32 * NR * NB * 4
+    NR, NB, nrb, NT = 131072 // 16, 1024, 8, 131072 // 16 // 128
+    # causal: partial sums for key blocks j <= b only (a packed triangle) and
+    # row stats for sub-tiles starting at or before the row
+    part = 32 * NB * (NB + 1) // 2 * nrb * 4
+    stats = 32 * (NT * NR - 128 * NT * (NT - 1) // 2) * 8
+    assert n == (part + 255) // 256 * 256 + stats
+    assert n < 0.52 * (32 * NR * NB * 4 + 32 * NR * NT * 8)   # about half the square
+    rc, n_full = _score_ws(_dims(hq=32, hkv=8, seq=131072, causal=0), 128, 16)
+    assert rc == 0 and n_full == 32 * NR * NB * 4 + 32 * NR * NT * 8
     lay = B.forward_layout(d, 128, 16)
     assert lay["scores"] == 0 and lay["idx"] >= 32 * NB * NB * 4
     assert all(v % 256 == 0 for v in lay.values())

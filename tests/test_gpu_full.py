@@ -184,6 +184,14 @@ def test_maximum_length_262144():
     check_properties(w, g)
     rows = (np.array([0, 0, 0], np.int32), np.array([0, 1024, 2047], np.int32))
     check_sampled(w, x, g, rows)
+    # the forward pass (finalize and selection fused) at 2048 blocks per row:
+    # bitwise the separate calls
+    o, lse, views = X.xattn_forward(g["q"], g["k"], g["v"], True, w.block, w.stride, w.tau,
+                                    want_lse=True)
+    torch.cuda.synchronize()
+    assert torch.equal(views["scores"], g["scores"]) and torch.equal(views["cnt"], g["cnt"])
+    assert torch.equal(o.view(torch.int16), g["o"].view(torch.int16))
+    assert torch.equal(lse, g["lse"])
 
 
 def test_zero_queries_tie_everywhere():

@@ -246,6 +246,32 @@ def test_forward_end_to_end_small(causal, S, kind):
     assert mx <= OUT_MAX_ABS and mean <= OUT_MEAN_ABS
 
 
+@pytest.mark.parametrize("L,hq,hkv,S,causal", [
+    (128 * 37, 4, 2, 8, True), (128 * 37, 2, 1, 4, False), (128 * 21, 2, 1, 1, True),
+    (8192, 2, 2, 64, True), (3072, 2, 1, 16, False), (128, 2, 1, 16, True)])
+def test_forward_equals_the_three_calls_bitwise(L, hq, hkv, S, causal):
+    """xattn_forward (partial sums, then finalize and selection fused in one
+    kernel, then attention) against xattn_score + xattn_select +
+    xattn_block_sparse_attn: scores, lists, outputs and LSE bitwise equal."""
+    x = _inputs(L, hq, hkv, seed=900 + S)
+    q, k, v = (dev_bf16(x[n]) for n in "qkv")
+    print(f"forward vs three calls L={L} S={S} causal={causal}", flush=True)
+    o1, l1, views = X.xattn_forward(q, k, v, causal=causal, stride=S, tau=0.9, want_lse=True)
+    sc = X.xattn_score(q, k, causal=causal, stride=S)
+    dims = X.make_dims(q, k, causal)
+    idx, cnt = X.xattn_select(sc, dims, 0.9)
+    o2, l2 = X.xattn_block_sparse_attn(q, k, v, idx, cnt, causal=causal)
+    torch.cuda.synchronize()
+    assert torch.equal(views["scores"], sc)
+    assert torch.equal(views["cnt"], cnt)
+    NB = L // 128
+    c = cnt.cpu().numpy().reshape(-1)
+    a, b = views["idx"].cpu().numpy().reshape(-1, NB), idx.cpu().numpy().reshape(-1, NB)
+    assert all(np.array_equal(a[r, :c[r]], b[r, :c[r]]) for r in range(len(c)))
+    assert torch.equal(o1.view(torch.int16), o2.view(torch.int16))
+    assert torch.equal(l1, l2)
+
+
 def test_repeated_calls_are_bitwise_deterministic():
     L, hq, hkv = 2048, 4, 2
     x = _inputs(L, hq, hkv, seed=501)
