@@ -303,8 +303,8 @@ int xattn_forward(const void* q, const void* k, const void* v, const xattn_dims*
   int32_t* idx = (int32_t*)(ws + o_idx);
   int32_t* cnt = (int32_t*)(ws + o_cnt);
   hipStream_t st = (hipStream_t)stream;
-  hipError_t e = launch_score_partials(q, k, s, stride, nullptr, ws + o_scr, st);
-  if (e == hipSuccess) e = launch_finalize_select(s, stride, ws + o_scr, tau, sc, idx, cnt, st);
+  hipError_t e = launch_score(q, k, s, stride, nullptr, sc, ws + o_scr, st);
+  if (e == hipSuccess) e = launch_select(sc, s, uniform_threshold(s, tau), idx, cnt, st);
   if (e == hipSuccess) e = launch_attn(q, k, v, s, idx, cnt, false, o, lse, st);
   return hip_status(e, "xattn_forward launch");
 }

@@ -80,16 +80,12 @@ struct SubRowPairing {
 hipError_t launch_score(const void* q, const void* k, const XattnShape& s, int stride,
                         const int32_t* qsub, float* scores, void* scratch, hipStream_t st);
 size_t score_scratch_bytes(const XattnShape& s, int stride);
-// The scoring in two parts: the partial sums and tile statistics into the
-// scratch, and (launch_finalize_select) the scores of each row computed from
-// them and selected in the same kernel.
+// Views of the scoring scratch: partial block masses and row statistics.
 struct ScoreScratch {
   float* part;   // partial block masses (layout in score_rows.h)
   float* stats;  // float2 (max, sum) per reduced row and column sub-tile
 };
 ScoreScratch score_scratch_views(const XattnShape& s, int stride, void* scratch);
-hipError_t launch_score_partials(const void* q, const void* k, const XattnShape& s, int stride,
-                                 const int32_t* qsub, void* scratch, hipStream_t st);
 // Selection rule of one launch: find_blocks with a threshold per head, or a
 // fixed block count per head (Top-K) or fraction of the candidates
 // (Top-Ratio). Passed by value as a kernel argument; with uniform != 0 every
@@ -103,11 +99,6 @@ struct SelectParams {
 };
 hipError_t launch_select(const float* scores, const XattnShape& s, const SelectParams& p,
                          int32_t* idx, int32_t* cnt, hipStream_t st);
-// Finalize + threshold selection of every row in one kernel (the forward
-// pass): scores are computed from the scoring scratch into LDS, written to
-// `scores` for the caller, and selected without being read back.
-hipError_t launch_finalize_select(const XattnShape& s, int stride, void* scratch, float tau,
-                                  float* scores, int32_t* idx, int32_t* cnt, hipStream_t st);
 size_t head_error_scratch_bytes(const XattnShape& s);
 hipError_t launch_head_error(const void* o, const void* o_ref, const XattnShape& s, double* err,
                              void* scratch, bool mean_over_batch, hipStream_t st);

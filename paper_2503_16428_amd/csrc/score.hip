@@ -407,7 +407,8 @@ ScoreScratch score_scratch_views(const XattnShape& s, int stride, void* scratch)
   return v;
 }
 
-hipError_t launch_score_partials(const void* q, const void* k, const XattnShape& s, int stride,
+// The partial-sum kernel of xattn_score (the first of its two launches).
+static hipError_t launch_score_partials(const void* q, const void* k, const XattnShape& s, int stride,
                                  const int32_t* qsub, void* scratch, hipStream_t st) {
   SubRowPairing pr;
   for (int t = 0; t < stride; ++t) pr.q[t] = qsub ? qsub[t] : stride - 1 - t;

@@ -1,8 +1,7 @@
 // Scoring scratch layout and the per-row finalisation of the block scores
 // (XAttention Sec. 3.2, Algorithm 1: reduced-row softmax, then the mean over
-// each query block's B/S reduced rows of the per-key-block sums). Shared by
-// the scoring kernels (score.hip) and the fused finalise + selection of the
-// forward pass (select.hip), so both produce bitwise the same scores.
+// each query block's B/S reduced rows of the per-key-block sums). Used by the
+// scoring kernels (score.hip); the layout functions are host-callable too.
 #pragma once
 
 #include "common.h"
@@ -61,18 +60,18 @@ struct FinalizeLds {
 //   f[r][t] = 2^(m[t][R] - m_R) / l_R,
 //   out[j] = (1/nrb) sum_r part[j][r] f[r][t(j)]   for the candidates j,
 //   out[j] = 0 for the other j < NB (causal: j > b).
-// The (r, t) stats are read r-fastest into LDS; one wave per row reduces them
-// in a fixed order. The row's partial-sum slab [j][r] is streamed as float4
-// (or float2 when nrb = 2), kFinUnroll loads in flight per thread; the nrb / 4
+// The (r, t) stats are read r-fastest (the nrb rows of one sub-tile are
+// adjacent in memory) into LDS; one wave per reduced row reduces them in a
+// fixed order. The row's partial-sum slab [j][r] is streamed as float4 (or
+// float2 when nrb = 2), kFinUnroll loads in flight per thread; the nrb / 4
 // lanes of one block then reduce with shuffles in a fixed order. Rows whose
 // stats exceed the LDS stage use the same arithmetic with the stats read from
-// global memory. Called by all kFinThreads threads of the workgroup; out may
-// point to global memory or LDS.
+// global memory. Called by all kFinThreads threads of the workgroup.
 template <bool CAUSAL>
 __device__ __forceinline__ void finalize_row(const float* __restrict__ part,
                                              const float2* __restrict__ stats, int NR, int NB,
-                                             int NT, int nrb, int h, int b, float* out,
-                                             FinalizeLds& L) {
+                                             int NT, int nrb, int h, int b,
+                                             float* __restrict__ out, FinalizeLds& L) {
   const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
   const int ncand = CAUSAL ? b + 1 : NB;
   const int tn = CAUSAL ? (b * nrb) / kTsub + 1 : NT;  // sub-tiles of this row's stats

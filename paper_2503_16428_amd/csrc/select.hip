@@ -19,7 +19,6 @@
 // the few values still inside the search interval are gathered one per lane,
 // so the remaining steps no longer scan every candidate.
 #include "common.h"
-#include "score_rows.h"
 
 using namespace xattn;
 
@@ -228,67 +227,7 @@ hipError_t launch_npl(const float* scores, const XattnShape& s, const SelectPara
   return hipGetLastError();
 }
 
-// The forward pass's finalize + selection: one workgroup per (head, query
-// block) row computes the row's scores from the scoring scratch into LDS
-// (finalize_row, the arithmetic of score_finalize), writes them out for the
-// caller, and its first wave selects from LDS (select_row, the arithmetic of
-// select_kernel with one threshold): the same scores and lists as the two
-// kernels, without reading the scores back from memory.
-template <int NPL, bool CAUSAL>
-__global__ __launch_bounds__(kFinThreads) void finalize_select_kernel(
-    const float* __restrict__ part, const float2* __restrict__ stats, int NR, int NB, int NT,
-    int nrb, float tau, float* __restrict__ scores, int32_t* __restrict__ idx,
-    int32_t* __restrict__ cnt) {
-  __shared__ FinalizeLds fin;
-  __shared__ float srow[64 * NPL];
-  __shared__ uint64_t stage[64];
-  const int row = blockIdx.x;
-  const int h = row / NB, b = row % NB;
-  finalize_row<CAUSAL>(part, stats, NR, NB, NT, nrb, h, b, srow, fin);
-  __syncthreads();
-  float* out = scores + (size_t)row * NB;
-  for (int j = threadIdx.x; j < NB; j += kFinThreads) out[j] = srow[j];
-  if (threadIdx.x >= 64) return;  // the first wave selects
-  const int lane = threadIdx.x;
-  const int m = CAUSAL ? b + 1 : NB;
-  int32_t* o = idx + (size_t)row * NB;
-  if (tau >= 1.f) {
-    for (int j = lane; j < m; j += 64) o[j] = j;
-    if (lane == 0) cnt[row] = m;
-    return;
-  }
-  select_row_sized<NPL, false>(srow, m, tau, 0, lane, o, cnt + row, stage);
-}
-
-template <int NPL>
-hipError_t launch_fs_npl(const XattnShape& s, int stride, const ScoreScratch& v, float tau,
-                         float* scores, int32_t* idx, int32_t* cnt, hipStream_t st) {
-  const int NR = s.seq / stride, NB = s.NB(), NT = (NR + kTsub - 1) / kTsub;
-  const int nrb = kBlock / stride;
-  const dim3 grid(s.HQ() * NB);
-  if (s.causal)
-    hipLaunchKernelGGL((finalize_select_kernel<NPL, true>), grid, dim3(kFinThreads), 0, st,
-                       v.part, (const float2*)v.stats, NR, NB, NT, nrb, tau, scores, idx, cnt);
-  else
-    hipLaunchKernelGGL((finalize_select_kernel<NPL, false>), grid, dim3(kFinThreads), 0, st,
-                       v.part, (const float2*)v.stats, NR, NB, NT, nrb, tau, scores, idx, cnt);
-  return hipGetLastError();
-}
-
 }  // namespace
-
-hipError_t launch_finalize_select(const XattnShape& s, int stride, void* scratch, float tau,
-                                  float* scores, int32_t* idx, int32_t* cnt, hipStream_t st) {
-  const ScoreScratch v = score_scratch_views(s, stride, scratch);
-  const int NB = s.NB();
-  if (NB <= 64) return launch_fs_npl<1>(s, stride, v, tau, scores, idx, cnt, st);
-  if (NB <= 128) return launch_fs_npl<2>(s, stride, v, tau, scores, idx, cnt, st);
-  if (NB <= 256) return launch_fs_npl<4>(s, stride, v, tau, scores, idx, cnt, st);
-  if (NB <= 512) return launch_fs_npl<8>(s, stride, v, tau, scores, idx, cnt, st);
-  if (NB <= 1024) return launch_fs_npl<16>(s, stride, v, tau, scores, idx, cnt, st);
-  if (NB <= 2048) return launch_fs_npl<32>(s, stride, v, tau, scores, idx, cnt, st);
-  return hipErrorInvalidValue;
-}
 
 hipError_t launch_select(const float* scores, const XattnShape& s, const SelectParams& p,
                          int32_t* idx, int32_t* cnt, hipStream_t st) {

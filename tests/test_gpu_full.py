@@ -184,8 +184,7 @@ def test_maximum_length_262144():
     check_properties(w, g)
     rows = (np.array([0, 0, 0], np.int32), np.array([0, 1024, 2047], np.int32))
     check_sampled(w, x, g, rows)
-    # the forward pass (finalize and selection fused) at 2048 blocks per row:
-    # bitwise the separate calls
+    # the forward pass at 2048 blocks per row: bitwise the separate calls
     o, lse, views = X.xattn_forward(g["q"], g["k"], g["v"], True, w.block, w.stride, w.tau,
                                     want_lse=True)
     torch.cuda.synchronize()

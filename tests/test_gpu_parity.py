@@ -250,9 +250,10 @@ def test_forward_end_to_end_small(causal, S, kind):
     (128 * 37, 4, 2, 8, True), (128 * 37, 2, 1, 4, False), (128 * 21, 2, 1, 1, True),
     (8192, 2, 2, 64, True), (3072, 2, 1, 16, False), (128, 2, 1, 16, True)])
 def test_forward_equals_the_three_calls_bitwise(L, hq, hkv, S, causal):
-    """xattn_forward (partial sums, then finalize and selection fused in one
-    kernel, then attention) against xattn_score + xattn_select +
-    xattn_block_sparse_attn: scores, lists, outputs and LSE bitwise equal."""
+    """xattn_forward (its workspace holding the packed scoring scratch behind
+    the scores and lists) against xattn_score + xattn_select +
+    xattn_block_sparse_attn with their own buffers: scores, lists, outputs and
+    LSE bitwise equal."""
     x = _inputs(L, hq, hkv, seed=900 + S)
     q, k, v = (dev_bf16(x[n]) for n in "qkv")
     print(f"forward vs three calls L={L} S={S} causal={causal}", flush=True)
