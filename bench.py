@@ -17,8 +17,8 @@ and their wall time (flushes included) is reported beside them.
 Prints ONE JSON line: ms per layer and dense-equivalent TFLOP/s (the value),
 per-stage times, density, speedup over the library's own dense mode, the MFMA
 roofline of the dominant kernel with its measured traffic, the random-block
-gather rate of the attention's load pattern, the shader clock and software
-versions, and the CPU oracle baseline on a sample.
+gather rate of the attention's load pattern, software versions, and the CPU
+oracle baseline on a sample.
 """
 from __future__ import annotations
 
@@ -208,51 +208,6 @@ def cpu_info():
     return {"cpu_model": model, "affinity_cpus": len(os.sched_getaffinity(0))}
 
 
-class ShaderClock:
-    """Mean shader clock per XCD over the timed region: the probe library's
-    clock kernel (64 workgroups, so every XCD) runs on the launch stream
-    right before the first and right after the last timed step and reads the
-    shader-cycle and constant-rate counters; per XCD, clock = cycles / (ticks
-    / tick rate)."""
-
-    def __init__(self, stream, n_wg=64):
-        import torch
-        from paper_2503_16428_amd import build as B
-        self.stream, self.n_wg, self.error = stream, n_wg, None
-        self.buf = torch.zeros((2, 3 * n_wg), dtype=torch.int64, device="cuda")
-        try:
-            self.lib = ctypes.CDLL(B.PROBE_LIB)
-            self.lib.xattn_probe_clock.argtypes = [ctypes.c_void_p, ctypes.c_int, ctypes.c_void_p]
-            self.khz = self.lib.xattn_probe_wall_clock_khz()
-        except OSError as e:
-            self.lib, self.error = None, f"probe library: {e}"
-
-    def sample(self, i):
-        if self.lib is None:
-            return
-        rc = self.lib.xattn_probe_clock(ctypes.c_void_p(self.buf[i].data_ptr()), self.n_wg,
-                                        ctypes.c_void_p(self.stream.cuda_stream))
-        if rc != 0:
-            self.error = f"clock probe launch failed ({rc})"
-
-    def result(self):
-        if self.lib is None or self.error or not self.khz:
-            return {"shader_clock_mhz": None, "error": self.error or "no tick rate"}
-        b = self.buf.cpu().numpy().reshape(2, self.n_wg, 3)
-        per = {}
-        for x in sorted(set(b[0, :, 0].tolist()) & set(b[1, :, 0].tolist())):
-            r0 = b[0][b[0, :, 0] == x][0]
-            r1 = b[1][b[1, :, 0] == x][0]
-            ticks = float(r1[2] - r0[2])
-            if ticks > 0:
-                per[int(x)] = (r1[1] - r0[1]) / (ticks / (self.khz * 1e3)) / 1e6
-        mhz = [per[x] for x in sorted(per)]
-        return {"shader_clock_mhz": round(float(np.mean(mhz)), 1) if mhz else None,
-                "per_xcd_mhz": [round(m, 1) for m in mhz],
-                "source": "s_memtime / s_memrealtime across the timed region",
-                "tick_rate_khz": self.khz}
-
-
 # ---------------------------------------------------------------- GPU legs
 
 
@@ -278,11 +233,10 @@ class Flusher:
             self.buf.fill_(self.n)
 
 
-def time_steps(stages, steps, warmup, stream, flush, clock=None):
+def time_steps(stages, steps, warmup, stream, flush):
     """Run warmup untimed steps, then `steps` timed ones (flush before each,
-    HIP events around each stage on the launch stream; the shader clock
-    sampled before the first and after the last). Returns (per-stage event
-    times [steps][n_stages] in ms, wall seconds of the timed steps)."""
+    HIP events around each stage on the launch stream). Returns (per-stage
+    event times [steps][n_stages] in ms, wall seconds of the timed steps)."""
     import torch
     for _ in range(warmup):
         for f in stages:
@@ -291,16 +245,12 @@ def time_steps(stages, steps, warmup, stream, flush, clock=None):
     evs = [[torch.cuda.Event(enable_timing=True) for _ in range(len(stages) + 1)]
            for _ in range(steps)]
     t0 = time.perf_counter()
-    if clock is not None:
-        clock.sample(0)
     for i in range(steps):
         flush()
         evs[i][0].record(stream)
         for j, f in enumerate(stages):
             f()
             evs[i][j + 1].record(stream)
-    if clock is not None:
-        clock.sample(1)
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
     st = np.array([[e[j].elapsed_time(e[j + 1]) for j in range(len(stages))] for e in evs])
@@ -415,7 +365,6 @@ def sweep_main(a, w, q, k, v, dims, stream, flush, x):
     o = torch.empty_like(q)
     points = []
     dflops = dense_flops(w)
-    clocks = []
     for tau, S in W.C4_SWEEP:
         wp = w.with_(tau=tau, stride=S)
         ws = torch.empty(X.score_workspace_size(dims, w.block, S), dtype=torch.uint8,
@@ -426,10 +375,7 @@ def sweep_main(a, w, q, k, v, dims, stream, flush, x):
             lambda: X.xattn_block_sparse_attn(q, k, v, idx, cnt, w.causal, w.block, o=o,
                                               want_lse=False),
         ]
-        clock = ShaderClock(stream)
-        st, wall = time_steps(stages, a.steps, a.warmup, stream, flush, clock)
-        clk = clock.result()
-        clocks.append(clk["shader_clock_mhz"])
+        st, wall = time_steps(stages, a.steps, a.warmup, stream, flush)
         t_score, t_select, t_attn = (median(st[:, j]) for j in range(3))
         ms = median(st.sum(1))
         c = cnt.cpu().numpy().astype(np.int64)
@@ -441,7 +387,7 @@ def sweep_main(a, w, q, k, v, dims, stream, flush, x):
             "tau": tau, "stride": S, "ms_per_step": round(ms, 4),
             "stages_ms": {"score": round(t_score, 4), "select": round(t_select, 4),
                           "attn": round(t_attn, 4)},
-            "density": round(dens, 5), "shader_clock_mhz": clk["shader_clock_mhz"],
+            "density": round(dens, 5),
             "dense_equiv_tflops": round(dflops / (ms * 1e-3) / 1e12, 1),
             "score_select_share": round((t_score + t_select) / (t_score + t_select + t_attn), 4),
             "roofline_attn": roofline_of("attn", attn_flops(blocks, w), t_attn, tr_a),
@@ -620,16 +566,14 @@ def main(argv=None):
 
     st, _ = time_steps([score, select, attend], a.steps, a.warmup, stream, flush)
     t_score, t_select, t_attn = (median(st[:, j]) for j in range(3))
-    clock = ShaderClock(stream)
     if fused:
-        stf, wall = time_steps([forward], a.steps, a.warmup, stream, flush, clock)
+        stf, wall = time_steps([forward], a.steps, a.warmup, stream, flush)
         ms_step = median(stf[:, 0])
         mean_step = float(stf[:, 0].mean())
     else:
-        st, wall = time_steps([score, select, attend], a.steps, 0, stream, flush, clock)
+        st, wall = time_steps([score, select, attend], a.steps, 0, stream, flush)
         ms_step = median(st.sum(1))
         mean_step = float(st.sum(1).mean())
-    clk = clock.result()
     print(f"# timed {a.steps} steps in {wall:.2f} s", file=sys.stderr, flush=True)
 
     c = cnt.cpu().numpy().astype(np.int64)
@@ -715,7 +659,6 @@ def main(argv=None):
         "roofline_other": roofline_of(other, kernels[other][0], kernels[other][1],
                                       other_traffic),
         "gather_probe": probe,
-        "clock": clk,
         "env": env_info(),
         "cpu_baseline": cpu,
     }

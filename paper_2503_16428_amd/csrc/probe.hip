@@ -1,4 +1,4 @@
-// Measurement probes (not part of the XAttention ABI; built into their own
+// Measurement probe (not part of the XAttention ABI; built into its own
 // library, libxattn_probe.so, and used by the benchmark only).
 //
 // xattn_probe_gather: the data movement of the block-sparse attention kernel
@@ -9,11 +9,6 @@
 // and fence-free barriers, so the rate it reaches is the rate at which that
 // load pattern can feed the attention kernel from wherever the blocks live
 // (L2, Infinity Cache or HBM, depending on the buffer size).
-//
-// xattn_probe_clock: per workgroup, the XCD it runs on and two counters read
-// back to back, the shader-clock cycle counter (s_memtime) and the constant-
-// rate counter (s_memrealtime). Two samples bracketing a timed region give
-// each XCD's mean shader clock over it: cycles / (ticks / tick rate).
 #include <hip/hip_runtime.h>
 
 #include <cstddef>
@@ -65,36 +60,7 @@ __global__ __launch_bounds__(kThreads, 2) void gather_probe_kernel(
   if (threadIdx.x == 0) sink[blockIdx.x] = lds[(blockIdx.x * 97) & (2 * 2 * 64 * 128 - 1)];
 }
 
-__global__ __launch_bounds__(64) void clock_probe_kernel(uint64_t* __restrict__ out) {
-  if (threadIdx.x == 0) {
-    uint32_t xcc;
-    asm volatile("s_getreg_b32 %0, hwreg(HW_REG_XCC_ID)" : "=s"(xcc));
-    const uint64_t cycles = __builtin_amdgcn_s_memtime();
-    const uint64_t ticks = __builtin_amdgcn_s_memrealtime();
-    out[3 * blockIdx.x] = xcc & 0xFu;
-    out[3 * blockIdx.x + 1] = cycles;
-    out[3 * blockIdx.x + 2] = ticks;
-  }
-}
-
 }  // namespace
-
-// out: 3 * n_wg uint64 (device): per workgroup (XCD id, shader cycles,
-// constant-rate ticks). Returns a hipError_t as int.
-extern "C" int xattn_probe_clock(uint64_t* out, int n_wg, void* stream) {
-  if (!out || n_wg < 1) return (int)hipErrorInvalidValue;
-  hipLaunchKernelGGL(clock_probe_kernel, dim3(n_wg), dim3(64), 0, (hipStream_t)stream, out);
-  return (int)hipGetLastError();
-}
-
-// Tick rate of the constant-rate counter of the current device, in kHz
-// (0 if the runtime does not report it).
-extern "C" int xattn_probe_wall_clock_khz(void) {
-  int dev = 0, khz = 0;
-  if (hipGetDevice(&dev) != hipSuccess) return 0;
-  if (hipDeviceGetAttribute(&khz, hipDeviceAttributeWallClockRate, dev) != hipSuccess) return 0;
-  return khz;
-}
 
 // buf: nblk 64 KB blocks (device); blocks: n_wg * per_wg block indices
 // (device int32, clamped to [0, nblk)); sink: n_wg uint32 (device). Returns
