@@ -555,8 +555,8 @@ def main(argv=None):
     # the step: xattn_forward (scoring, selection, attention in one call) where
     # it applies (one threshold, antidiagonal pattern); the stage times come
     # from the same kernels launched as three separate calls
-    fused = a.select_mode == "threshold" and a.pattern == "antidiagonal"
-    if fused:
+    one_call = a.select_mode == "threshold" and a.pattern == "antidiagonal"
+    if one_call:
         fws = torch.empty(X.forward_workspace_size(dims, w.block, w.stride), dtype=torch.uint8,
                           device=dev)
         of = torch.empty_like(q)
@@ -566,7 +566,7 @@ def main(argv=None):
 
     st, _ = time_steps([score, select, attend], a.steps, a.warmup, stream, flush)
     t_score, t_select, t_attn = (median(st[:, j]) for j in range(3))
-    if fused:
+    if one_call:
         stf, wall = time_steps([forward], a.steps, a.warmup, stream, flush)
         ms_step = median(stf[:, 0])
         mean_step = float(stf[:, 0].mean())
@@ -640,7 +640,7 @@ def main(argv=None):
                        "topk": {"k_blocks": a.topk},
                        "ratio": {"ratio": a.ratio}}[a.select_mode] | {"mode": a.select_mode}})),
         "protocol": protocol_note(a),
-        "step": ("xattn_forward" if fused
+        "step": ("xattn_forward" if one_call
                  else "xattn_score / xattn_select* / xattn_block_sparse_attn"),
         "wall_ms_per_step_incl_flush": round(wall * 1e3 / a.steps, 4),
         "mean_ms_per_step": round(mean_step, 4),

@@ -68,3 +68,38 @@ def test_noalloc_rejects_problems_beyond_the_static_scratch():
     with pytest.raises(B.XAttnError) as e:
         X.xattn_forward_noalloc(q, kv, kv, o, None, True, 128, 8, 0.9)
     assert e.value.status == B.XATTN_ERR_UNSUPPORTED and "scratch" in str(e.value)
+
+
+def test_noalloc_forward_captured_in_a_graph_replays_like_eager():
+    """The no-allocation forward is what code under graph capture calls: a
+    captured call, replayed on new inputs copied into the captured buffers
+    (eager work and synchronisation between replays), gives bitwise the
+    eager xattn_forward result every time."""
+    w, x, (q, k, v) = _case(4096, 4, 2, 8, True, 81)
+    o = torch.empty_like(q)
+    lse = torch.empty((4, 4096), dtype=torch.float32, device="cuda")
+    s = torch.cuda.Stream()
+    s.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(s):
+        X.xattn_forward_noalloc(q, k, v, o, lse, True, 128, 8, 0.9, stream=s)  # outside capture
+    torch.cuda.current_stream().wait_stream(s)
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    print("capturing xattn_forward_noalloc", flush=True)
+    with torch.cuda.graph(g):
+        X.xattn_forward_noalloc(q, k, v, o, lse, True, 128, 8, 0.9)
+    torch.cuda.synchronize()
+    for seed in (82, 83, 84):
+        _, _, (qn, kn, vn) = _case(4096, 4, 2, 8, True, seed)
+        q.copy_(qn)
+        k.copy_(kn)
+        v.copy_(vn)
+        torch.cuda.synchronize()
+        print(f"replay with inputs of seed {seed}", flush=True)
+        g.replay()
+        torch.cuda.synchronize()
+        got_o, got_lse = o.clone(), lse.clone()
+        want_o, want_lse, _ = X.xattn_forward(qn, kn, vn, True, 128, 8, 0.9, want_lse=True)
+        torch.cuda.synchronize()
+        assert torch.equal(got_o.view(torch.int16), want_o.view(torch.int16)), seed
+        assert torch.equal(got_lse, want_lse), seed
