@@ -89,7 +89,7 @@ def parse(argv=None):
     ap.add_argument("--no-flush", action="store_true",
                     help="skip the 512 MB cache-evicting write before each timed step")
     ap.add_argument("--no-probe", action="store_true",
-                    help="skip the random 64 KB block gather probe")
+                    help="skip the probes (random 64 KB block gather; library GEMM of the scoring shape)")
     ap.add_argument("--dense-steps", type=int, default=3)
     ap.add_argument("--copy-calibration", action="store_true",
                     help="after the timed region, copy a 256 MiB buffer once (a plain copy "
@@ -303,6 +303,42 @@ def gather_probe(stream, per_wg=64, n_wg=4096, seed=7):
                       "TBps": round(out["bytes_per_launch"] / (ms * 1e-3) / 1e12, 3)}
         del buf, blocks
     return out
+
+
+def gemm_probe(stream, w, score_tflops):
+    """Rate of a plain library GEMM with the reduced product's operand shapes
+    (torch.matmul in bf16, served by hipBLASLt): per head, (L/S x S d) times
+    (S d x L/S), the full square with a bf16 output. It measures what this
+    GPU's matrix cores sustain on that shape under its power limit, as a
+    practical ceiling beside the nominal peak for the scoring kernel (which
+    computes the causal half and fuses the softmax epilogue instead of
+    writing the product)."""
+    import torch
+    m, kd, heads = w.seq // w.stride, w.stride * w.head_dim, w.hq * w.batch
+    g = torch.Generator(device="cuda").manual_seed(11)
+    with torch.cuda.stream(stream):
+        A = torch.randn((heads, m, kd), generator=g, device="cuda").to(torch.bfloat16)
+        B = torch.randn((heads, kd, m), generator=g, device="cuda").to(torch.bfloat16)
+        C = torch.empty((heads, m, m), device="cuda", dtype=torch.bfloat16)
+        for _ in range(3):
+            torch.matmul(A, B, out=C)
+        torch.cuda.synchronize()
+        ts = []
+        for _ in range(5):
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record(stream)
+            torch.matmul(A, B, out=C)
+            e1.record(stream)
+            torch.cuda.synchronize()
+            ts.append(e0.elapsed_time(e1))
+    del A, B, C
+    ms = median(ts)
+    tflops = 2.0 * heads * m * m * kd / (ms * 1e-3) / 1e12
+    return {"op": "torch.matmul bf16 (hipBLASLt): per head (L/S x S*d) @ (S*d x L/S), "
+                  "full square, bf16 output",
+            "shape": [heads, m, kd, m], "ms": round(ms, 4), "TFLOPs": round(tflops, 1),
+            "frac_of_bf16_peak": round(tflops / PEAK_BF16_TFLOPS, 4),
+            "score_frac_of_library": round(score_tflops / tflops, 4)}
 
 
 def cpu_baseline(w, x, n_rows: int):
@@ -599,9 +635,10 @@ def main(argv=None):
         dense_ms = median(dst_[:, 0])
         print(f"# dense mode {dense_ms:.2f} ms", file=sys.stderr, flush=True)
 
-    probe = None
+    probe = gemm = None
     if not a.no_probe:
         probe = gather_probe(stream)
+        gemm = gemm_probe(stream, w, s_flops / (t_score * 1e-3) / 1e12)
 
     # dominant kernel of the step and its MFMA roofline (both GEMM-shaped
     # kernels are priced against the bf16 peak; the measured traffic sits
@@ -659,6 +696,7 @@ def main(argv=None):
         "roofline_other": roofline_of(other, kernels[other][0], kernels[other][1],
                                       other_traffic),
         "gather_probe": probe,
+        "gemm_probe": gemm,
         "env": env_info(),
         "cpu_baseline": cpu,
     }
