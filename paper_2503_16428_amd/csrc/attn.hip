@@ -321,11 +321,10 @@ __device__ __forceinline__ void attn_body(
     mpre = lane_max(sn);  // for the next step, beside the last PV MFMAs
     asm volatile("" ::"v"(mpre));  // (not sunk past the next step's mask branch)
     // Schedule: LDS reads run two MFMAs ahead of their use. The softmax work
-    // is spread over all 32 MFMAs so that no MFMA waits for more than its own
-    // 32 cycles of VALU (an exp2 issues in 16, other VALU in 4): the QK^T
-    // MFMAs carry the exponentials of PV steps 0-2 (1.5 per MFMA, with their
-    // fma / add / convert), the first 8 PV MFMAs those of PV step 3, the last
-    // 8 the max of S(i+1).
+    // is spread over all 32 MFMAs so that the VALU between two MFMAs stays
+    // well inside one MFMA's 32 cycles: the QK^T MFMAs carry the exponentials
+    // of PV steps 0-2 (1.5 per MFMA, with their fma / add / convert), the
+    // first 8 PV MFMAs those of PV step 3, the last 8 the max of S(i+1).
     __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);    // DS read (K operand)
 #pragma unroll
     for (int t = 0; t < 16; ++t) {
