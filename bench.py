@@ -89,7 +89,8 @@ def parse(argv=None):
     ap.add_argument("--no-flush", action="store_true",
                     help="skip the 512 MB cache-evicting write before each timed step")
     ap.add_argument("--no-probe", action="store_true",
-                    help="skip the probes (random 64 KB block gather; library GEMM of the scoring shape)")
+                    help="skip the probes (random 64 KB block gather; library GEMM of the scoring "
+                         "shape; the library's dense attention)")
     ap.add_argument("--dense-steps", type=int, default=3)
     ap.add_argument("--copy-calibration", action="store_true",
                     help="after the timed region, copy a 256 MiB buffer once (a plain copy "
@@ -339,6 +340,46 @@ def gemm_probe(stream, w, score_tflops):
             "shape": [heads, m, kd, m], "ms": round(ms, 4), "TFLOPs": round(tflops, 1),
             "frac_of_bf16_peak": round(tflops / PEAK_BF16_TFLOPS, 4),
             "score_frac_of_library": round(score_tflops / tflops, 4)}
+
+
+def library_dense_probe(stream, w, q, k, v, dense_ms, ms_step, o_dense):
+    """The vendor's dense attention on the same layer, for context: torch's
+    scaled_dot_product_attention restricted to its flash backend (no fallback
+    to the math path), K/V expanded to the query heads for GQA. Returns its
+    time, rate, the speedups over it, and its largest difference from this
+    library's dense output (o_dense, when given)."""
+    import torch
+    import torch.nn.functional as F
+    from torch.nn.attention import SDPBackend, sdpa_kernel
+    G = w.hq // w.hkv
+    try:
+        with torch.cuda.stream(stream), sdpa_kernel([SDPBackend.FLASH_ATTENTION]):
+            qq = q.unsqueeze(0)
+            kk = k.repeat_interleave(G, dim=0).unsqueeze(0).contiguous()
+            vv = v.repeat_interleave(G, dim=0).unsqueeze(0).contiguous()
+            ref = F.scaled_dot_product_attention(qq, kk, vv, is_causal=w.causal)
+            torch.cuda.synchronize()
+            ts = []
+            for _ in range(3):
+                e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+                e0.record(stream)
+                ref = F.scaled_dot_product_attention(qq, kk, vv, is_causal=w.causal)
+                e1.record(stream)
+                torch.cuda.synchronize()
+                ts.append(e0.elapsed_time(e1))
+            diff = None
+            if o_dense is not None:
+                diff = float((ref[0].float() - o_dense.float()).abs().max().item())
+            del kk, vv, ref
+    except (RuntimeError, ValueError) as e:
+        return {"op": "torch SDPA, flash backend", "error": f"{type(e).__name__}: {str(e)[:160]}"}
+    ms = median(ts)
+    tflops = dense_flops(w) / (ms * 1e-3) / 1e12
+    return {"op": "torch SDPA, flash backend (K/V expanded for GQA)", "ms": round(ms, 3),
+            "TFLOPs": round(tflops, 1), "frac_of_bf16_peak": round(tflops / PEAK_BF16_TFLOPS, 4),
+            "speedup_of_layer_over_it": round(ms / ms_step, 3),
+            "own_dense_speedup_over_it": None if dense_ms is None else round(ms / dense_ms, 3),
+            "max_abs_diff_vs_own_dense": None if diff is None else round(diff, 5)}
 
 
 def cpu_baseline(w, x, n_rows: int):
@@ -635,10 +676,12 @@ def main(argv=None):
         dense_ms = median(dst_[:, 0])
         print(f"# dense mode {dense_ms:.2f} ms", file=sys.stderr, flush=True)
 
-    probe = gemm = None
+    probe = gemm = libdense = None
     if not a.no_probe:
         probe = gather_probe(stream)
         gemm = gemm_probe(stream, w, s_flops / (t_score * 1e-3) / 1e12)
+        libdense = library_dense_probe(stream, w, q, k, v, dense_ms, ms_step,
+                                       None if dense_ms is None else o)
 
     # dominant kernel of the step and its MFMA roofline (both GEMM-shaped
     # kernels are priced against the bf16 peak; the measured traffic sits
@@ -697,6 +740,7 @@ def main(argv=None):
                                       other_traffic),
         "gather_probe": probe,
         "gemm_probe": gemm,
+        "library_dense": libdense,
         "env": env_info(),
         "cpu_baseline": cpu,
     }
