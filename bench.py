@@ -16,9 +16,10 @@ and their wall time (flushes included) is reported beside them.
 
 Prints ONE JSON line: ms per layer and dense-equivalent TFLOP/s (the value),
 per-stage times, density, speedup over the library's own dense mode, the MFMA
-roofline of the dominant kernel with its measured traffic, the random-block
-gather rate of the attention's load pattern, software versions, and the CPU
-oracle baseline on a sample.
+roofline of the dominant kernel with its measured traffic, three probes for
+context (the random-block gather rate of the attention's load pattern, a
+library bf16 GEMM of the scoring's operand shapes, torch's flash attention on
+the same layer), software versions, and the CPU oracle baseline on a sample.
 """
 from __future__ import annotations
 
