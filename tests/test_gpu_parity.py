@@ -217,14 +217,19 @@ def test_select_on_oracle_scores_rounded_to_fp32():
         assert np.array_equal(gi[r, :gc[r]], oi[r, :oc[r]])
 
 
-@pytest.mark.parametrize("causal,S,kind", [(True, 8, "clustered"), (True, 16, "clustered_local"),
-                                           (False, 16, "clustered")])
-def test_forward_end_to_end_small(causal, S, kind):
-    L, hq, hkv, tau = 3072, 4, 2, 0.9
+@pytest.mark.parametrize("causal,S,kind,L,hq,hkv", [
+    (True, 8, "clustered", 3072, 4, 2), (True, 16, "clustered_local", 3072, 4, 2),
+    (False, 16, "clustered", 3072, 4, 2),
+    # query-head groups of 8 and 16, odd group counts, plain multi-head
+    (True, 8, "clustered", 2048, 8, 1), (True, 4, "clustered", 2048, 16, 2),
+    (True, 8, "clustered_local", 1536, 16, 1), (False, 8, "clustered", 1536, 6, 3),
+    (True, 16, "clustered", 2560, 3, 3)])
+def test_forward_end_to_end_small(causal, S, kind, L, hq, hkv):
+    tau = 0.9
     x = _inputs(L, hq, hkv, seed=401, kind=kind)
     NB = L // 128
     q, k, v = (dev_bf16(x[n]) for n in "qkv")
-    print(f"forward L={L} S={S} causal={causal} kind={kind}", flush=True)
+    print(f"forward L={L} hq={hq} hkv={hkv} S={S} causal={causal} kind={kind}", flush=True)
     o, _, views = X.xattn_forward(q, k, v, causal=causal, stride=S, tau=tau)
     torch.cuda.synchronize()
     f = oracle.forward_rows(x["q"], x["k"], x["v"], 128, S, tau, causal)
