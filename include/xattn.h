@@ -249,6 +249,9 @@ int xattn_forward_scheduled(const void *q, const void *k, const void *v,
  *                to M; the threshold of head h becomes t0 * 0.9^adjust[h]
  *   best         host double (output, may be NULL): D[heads][M]
  * On equal performance a head keeps fewer adjustments. Host only (no GPU).
+ * XATTN_ERR_ARG for a NULL table or adjust, heads < 1, max_adjust < 1, M
+ * outside [0, heads * max_adjust] or a non-finite entry; XATTN_ERR_UNSUPPORTED
+ * for tables above 2^26 entries or heads * max_adjust above 2^20.
  */
 int xattn_threshold_dp(const double *perf, int heads, int max_adjust, int adjustments,
                        int32_t *adjust, double *best);

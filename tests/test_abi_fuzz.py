@@ -75,7 +75,8 @@ def test_threshold_dp_rejects_or_runs(heads, max_adjust, adjustments):
     total = ctypes.c_double(0.0)
     rc = lib.xattn_threshold_dp(perf, heads, max_adjust, adjustments, adj, ctypes.byref(total))
     assert rc in CODES
-    assert (rc == B.XATTN_OK) == (adjustments <= heads * max_adjust)
+    # the documented contract: max_adjust >= 1 and M in [0, heads * max_adjust]
+    assert (rc == B.XATTN_OK) == (max_adjust >= 1 and adjustments <= heads * max_adjust)
     if rc == B.XATTN_OK:
         assert all(0 <= a <= max_adjust for a in adj)
         assert sum(adj) == adjustments
